@@ -1,0 +1,385 @@
+"""Pins of the float64 oracle against facts the paper and the mathematics fix.
+
+Each test names the pin it implements.  None of them re-types the oracle's own
+formula: they compare against a library routine (scipy's DCT), hand-derived
+values (tests/golden/), exact identities of the greedy step (App. E), closed
+forms on hand-solvable inputs, an independently written z-domain variant of
+Alg. 2 built on scipy's DCT, and brute-force optimal clustering.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.fft
+
+import oracle.kashin_ref as ref
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gauss(rng, b, n, std=1.0):
+    return rng.standard_normal((b, n)) * std
+
+
+# ----------------------------------------------------------------------------- eps
+def test_splitmix64_published_outputs():
+    vals = [int(line, 16) for line in open(os.path.join(GOLDEN, "splitmix64_seed0.txt"))
+            if line.strip() and not line.startswith("#")]
+    assert ref.splitmix64(0, 3) == vals
+
+
+def test_sign_mask_is_top_bit_and_balanced():
+    eps = ref.sign_mask(4096, 7)
+    raw = ref.splitmix64(7, 4096)
+    assert all((e == -1) == bool(v >> 63) for e, v in zip(eps, raw))
+    assert set(np.unique(eps)) == {-1, 1}
+    assert abs(int(eps.sum())) < 4 * math.sqrt(4096)
+
+
+# ----------------------------------------------------------------------------- DCT (T1, T2)
+def test_dct_golden_small():
+    lines = [l for l in open(os.path.join(GOLDEN, "dct2_ortho_small.txt")) if l.strip() and not l.startswith("#")]
+    i = 0
+    seen = 0
+    while i < len(lines):
+        n = int(lines[i]); i += 1
+        mat = np.array([[float(v) for v in lines[i + r].split()] for r in range(n)])
+        i += n
+        np.testing.assert_allclose(ref.dct2_matrix(n), mat, rtol=0, atol=1e-15)
+        seen += 1
+    assert seen == 2
+
+
+@pytest.mark.parametrize("n", [2, 3, 8, 12, 43, 64, 86, 96])
+def test_dct_matches_library(n, rng):
+    """T1: the explicit-cosine matrix equals scipy's orthonormal DCT-II."""
+    x = rng.standard_normal((5, n))
+    ours = x @ ref.dct2_matrix(n).T
+    lib = scipy.fft.dct(x, type=2, norm="ortho", axis=1)
+    np.testing.assert_allclose(ours, lib, rtol=0, atol=1e-13)
+    back = scipy.fft.idct(lib, type=2, norm="ortho", axis=1)
+    np.testing.assert_allclose(ours @ ref.dct2_matrix(n), back, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("n", [7, 64, 768])
+def test_dct_orthonormal_parseval(n, rng):
+    """T2: C C^T = I and ||C x|| = ||x||."""
+    c = ref.dct2_matrix(n)
+    np.testing.assert_allclose(c @ c.T, np.eye(n), rtol=0, atol=1e-12)
+    x = rng.standard_normal(n)
+    assert abs(np.linalg.norm(c @ x) - np.linalg.norm(x)) < 1e-12 * np.linalg.norm(x)
+
+
+# ----------------------------------------------------------------------------- P (T3)
+@pytest.mark.parametrize("n,seed", [(6, 1), (64, 2), (768, 3)])
+def test_p_symmetric_involution(n, seed):
+    """T3: P^T = P and P^2 = I (App. C, App. E)."""
+    p = ref.p_matrix(ref.sign_mask(n, seed))
+    np.testing.assert_allclose(p, p.T, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(p @ p, np.eye(n), rtol=0, atol=1e-12)
+
+
+def test_p_n2_by_hand():
+    """N = 2, eps = (+1, -1): C = [[1,1],[1,-1]]/sqrt2 gives P = [[0,1],[1,0]] (a swap)."""
+    p = ref.p_matrix(np.array([1, -1]))
+    np.testing.assert_allclose(p, [[0.0, 1.0], [1.0, 0.0]], atol=1e-15)
+    p = ref.p_matrix(np.array([1, 1]))
+    np.testing.assert_allclose(p, np.eye(2), atol=1e-15)
+
+
+@pytest.mark.parametrize("n", [16, 512])
+def test_apply_p_matches_library_pipeline(n, rng):
+    """P z = IDCT(eps * DCT(z)) via scipy equals the oracle's matrix application."""
+    eps = ref.sign_mask(n, 11)
+    z = rng.standard_normal((3, n))
+    lib = scipy.fft.idct(eps * scipy.fft.dct(z, norm="ortho", axis=1), norm="ortho", axis=1)
+    np.testing.assert_allclose(ref.apply_p(z, eps), lib, atol=1e-12)
+    np.testing.assert_allclose(ref.p_matrix(eps) @ z[0], lib[0], atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- Alg. 2
+@pytest.fixture(scope="module")
+def traced():
+    rng = np.random.default_rng(5)
+    n = 96
+    w = rng.standard_normal((6, n)) * 0.02
+    w[1] *= 50.0
+    w[2] = rng.standard_t(3, n)
+    eps = ref.sign_mask(n, 3)
+    out = ref.decompose(w, eps, 8, trace=True)
+    return w, eps, out
+
+
+def test_one_step_energy_identity(traced):
+    """T4 (App. E, one-step estimate): ||rho'||^2 = ||rho||^2 - 2 c ||x||_1 + c^2 nnz(x),
+    which is ||rho||^2 - ||x||_1^2 / N when x has no zero entries."""
+    w, eps, out = traced
+    tr = out["trace"]
+    n = w.shape[1]
+    pred = tr["r2_before"] - 2 * tr["c"] * tr["l1"] + tr["c"] ** 2 * tr["nnz"]
+    scale = tr["r2_before"][:, :1]
+    np.testing.assert_allclose(tr["r2_after"] / scale, pred / scale, rtol=0, atol=1e-12)
+    full = tr["nnz"] == n
+    pred2 = tr["r2_before"] - tr["l1"] ** 2 / n
+    assert np.allclose((tr["r2_after"] / scale)[full], (pred2 / scale)[full], rtol=0, atol=1e-12)
+
+
+def test_residual_monotone(traced):
+    """T5: every atomic step is non-expansive (App. E)."""
+    tr = traced[2]["trace"]
+    assert np.all(tr["r2_after"] <= tr["r2_before"] * (1 + 1e-12) + 1e-300)
+
+
+def test_coefficient_and_linf_bounds(traced):
+    """T6 (App. F): |lambda| <= ||rho||_2 / sqrt(N); ||u_k||_inf <= sum of u-step c's; same for vhat."""
+    w, eps, out = traced
+    tr = out["trace"]
+    n = w.shape[1]
+    assert np.all(tr["c"] <= np.sqrt(tr["r2_before"]) / math.sqrt(n) * (1 + 1e-12))
+    assert np.all(np.abs(out["u"]).max(axis=1) <= out["csum"][:, 0] * (1 + 1e-12))
+    assert np.all(np.abs(out["vhat"]).max(axis=1) <= out["csum"][:, 1] * (1 + 1e-12))
+    # ||P v||_inf bound of Thm. 2 is on P vhat's preimage: P(vhat) = v, and vhat itself is bounded.
+
+
+def test_reconstruction_identity(traced):
+    """T7: x = u_k + P vhat_k + r_k exactly (up to float64 rounding), Alg. 2 output."""
+    w, eps, out = traced
+    rec = out["u"] + ref.apply_p(out["vhat"], eps) + out["r"]
+    np.testing.assert_allclose(rec, w, rtol=0, atol=1e-13 * np.abs(w).max())
+
+
+def test_geometric_decay_and_floor(traced):
+    """T12 (Fig. 2 / Thm. 2 shape): block residuals fall geometrically (every block contracts)."""
+    w, eps, out = traced
+    tr = out["trace"]
+    r_blocks = np.sqrt(tr["r2_after"][:, 3::4])
+    r0 = np.linalg.norm(w, axis=1)
+    ratios = r_blocks / np.concatenate([r0[:, None], r_blocks[:, :-1]], axis=1)
+    assert np.all(ratios < 0.7)
+    assert np.all(r_blocks[:, -1] < 1e-4 * r0)
+
+
+def test_four_exact_values_after_one_block(rng):
+    """T8 (Sec. 3.1): after one block u takes only the values +-c1 +- c2 and vhat only +-c3 +- c4,
+    so the closed-form centres quantise both factors with zero error."""
+    n = 128
+    w = rng.standard_normal((4, n))
+    eps = ref.sign_mask(n, 9)
+    out = ref.decompose(w, eps, 1)
+    c = out["cstep"]
+    for b in range(4):
+        mags_u = np.unique(np.round(np.abs(out["u"][b]) / c[b, 0], 12))
+        expect_u = np.unique(np.round(np.array([c[b, 0] + c[b, 1], abs(c[b, 0] - c[b, 1])]) / c[b, 0], 12))
+        assert set(mags_u) <= set(expect_u)
+        mags_v = np.unique(np.round(np.abs(out["vhat"][b]) / c[b, 2], 12))
+        expect_v = np.unique(np.round(np.array([c[b, 2] + c[b, 3], abs(c[b, 2] - c[b, 3])]) / c[b, 2], 12))
+        assert set(mags_v) <= set(expect_v)
+    cu, cv, centers = ref.cluster2bit(out["u"], out["vhat"], out["cstep"], 0)
+    uq, vq = ref.dequantize(cu, cv, centers)
+    np.testing.assert_allclose(uq, out["u"], atol=1e-14)
+    np.testing.assert_allclose(vq, out["vhat"], atol=1e-14)
+
+
+def _zdomain_alg2(w, eps, k):
+    """Independent restatement of Alg. 2 that keeps z = P rho and uses P^2 = I
+    (rho - P d, then P of that, equals z - d), with P taken from scipy's DCT."""
+    def p(x):
+        return scipy.fft.idct(eps * scipy.fft.dct(x, norm="ortho", axis=1), norm="ortho", axis=1)
+    n = w.shape[1]
+    rho = w.copy()
+    u = np.zeros_like(w)
+    vh = np.zeros_like(w)
+    for _ in range(k):
+        for _ in range(2):
+            c = np.abs(rho).sum(1, keepdims=True) / n
+            d = np.sign(rho) * c
+            u += d
+            rho = rho - d
+        z = p(rho)
+        for _ in range(2):
+            c = np.abs(z).sum(1, keepdims=True) / n
+            d = np.sign(z) * c
+            vh += d
+            z = z - d
+        rho = p(z)
+    return u, vh, rho
+
+
+def test_literal_equals_zdomain_form(rng):
+    """T9: the literal Alg. 2 (P rho recomputed, rho -= P delta) equals the z-domain form."""
+    n = 64
+    w = rng.standard_normal((5, n))
+    eps = ref.sign_mask(n, 4)
+    out = ref.decompose(w, eps, 3)
+    u, vh, r = _zdomain_alg2(w, eps, 3)
+    np.testing.assert_allclose(out["u"], u, atol=1e-12)
+    np.testing.assert_allclose(out["vhat"], vh, atol=1e-12)
+    np.testing.assert_allclose(out["r"], r, atol=1e-12)
+
+
+def test_homogeneity_and_odd_symmetry(rng):
+    """T10: decompose(a w) = a decompose(w) for a > 0 (exact for powers of two) and
+    decompose(-w) = -decompose(w) (sign is odd, ||.||_1 is even)."""
+    n = 48
+    w = rng.standard_normal((3, n))
+    eps = ref.sign_mask(n, 8)
+    base = ref.decompose(w, eps, 4)
+    dbl = ref.decompose(4.0 * w, eps, 4)
+    neg = ref.decompose(-w, eps, 4)
+    for key in ("u", "vhat", "r"):
+        np.testing.assert_array_equal(dbl[key], 4.0 * base[key])
+        np.testing.assert_array_equal(neg[key], -base[key])
+    sc = ref.decompose(2.5 * w, eps, 4)
+    np.testing.assert_allclose(sc["u"], 2.5 * base["u"], rtol=1e-12, atol=1e-15)
+
+
+def test_hand_solvable_cube_vertex():
+    """T11: w = a s with s in {-1,+1}^N is a single atom of Q_N: the first u-step takes c = a
+    and leaves a zero residual, so u = w and vhat = r = 0."""
+    n = 16
+    s = np.where(np.arange(n) % 3 == 0, -1.0, 1.0)
+    w = 0.75 * s
+    out = ref.decompose(w, ref.sign_mask(n, 2), 2)
+    np.testing.assert_array_equal(out["u"][0], w)
+    assert not out["vhat"].any() and not out["r"].any()
+    np.testing.assert_array_equal(out["cstep"][0], [0.75, 0.0, 0.0, 0.0])
+
+
+def test_hand_solvable_zero_and_one_hot():
+    """T11: a zero row stays zero; a one-hot row a e_0 exercises sign(0) = 0 and the 1/N divisor:
+    step 1 gives c1 = a/N and rho_0 = a (1 - 1/N); step 2 gives c2 = a (1 - 1/N) / N."""
+    n = 10
+    eps = ref.sign_mask(n, 5)
+    z = ref.decompose(np.zeros(n), eps, 3)
+    assert not z["u"].any() and not z["vhat"].any() and not z["r"].any()
+    a = 3.0
+    w = np.zeros(n); w[0] = a
+    out = ref.decompose(w, eps, 1, trace=True)
+    c1 = a / n
+    c2 = a * (1 - 1 / n) / n
+    assert out["cstep"][0, 0] == pytest.approx(c1, rel=1e-15)
+    assert out["cstep"][0, 1] == pytest.approx(c2, rel=1e-15)
+    sg = out["trace"]["signs"][0]
+    assert sg[0, 0] == 1 and not sg[0, 1:].any()  # untouched zeros keep sign 0
+
+
+# ----------------------------------------------------------------------------- clustering (T13)
+def test_optimal4_bruteforce_vs_dp(rng):
+    x = rng.standard_normal(20)
+    bf = ref.optimal4_sse(x)
+    # run the DP branch on the same data by padding with copies of an existing value far away
+    # is not equivalent; instead check the DP on a larger sample against brute force over
+    # contiguous partitions computed here by exhaustive search of 3 cuts.
+    xs = np.sort(rng.standard_normal(30))
+    best = np.inf
+    for c1 in range(31):
+        for c2 in range(c1, 31):
+            for c3 in range(c2, 31):
+                tot = 0.0
+                for lo, hi in ((0, c1), (c1, c2), (c2, c3), (c3, 30)):
+                    if hi > lo:
+                        seg = xs[lo:hi]
+                        tot += ((seg - seg.mean()) ** 2).sum()
+                best = min(best, tot)
+    assert ref.optimal4_sse(xs) == pytest.approx(best, rel=1e-12)
+    assert bf <= ref.sse4(x, ref.closed_form_centers(0.5, 0.3)) + 1e-12
+
+
+def test_optimal4_known_cases():
+    assert ref.optimal4_sse(np.array([1.0, 1.0, 5.0, 5.0, 9.0, -3.0])) == pytest.approx(0.0)
+    assert ref.optimal4_sse(np.array([0.0, 1.0, 10.0, 20.0, 30.0])) == pytest.approx(0.5)
+
+
+def test_lloyd_between_closed_form_and_optimum(rng):
+    """T13: SSE_opt <= SSE_Lloyd(L) <= ... <= SSE_closed-form, on tiny decompositions (N = 16)
+    where the optimum is found by brute force."""
+    n = 16
+    eps = ref.sign_mask(n, 6)
+    w = rng.standard_normal((6, n))
+    d = ref.decompose(w, eps, 6)
+    q0 = ref.closed_form_centers(d["cstep"][:, 0], d["cstep"][:, 1])
+    for b in range(6):
+        x = d["u"][b]
+        opt = ref.optimal4_sse(x)
+        prev = ref.sse4(x, q0[b])
+        assert opt <= prev + 1e-12
+        for L in (1, 2, 5):
+            qL = ref.lloyd(x[None], q0[b:b + 1], L)[0]
+            cur = ref.sse4(x, qL)
+            assert opt - 1e-12 <= cur <= prev + 1e-12
+            prev = cur
+
+
+def test_assign_ties_go_low():
+    q = np.array([[-3.0, -1.0, 1.0, 3.0]])
+    x = np.array([[-2.0, 0.0, 2.0, -2.0000001, 2.0000001, 5.0, -5.0]])
+    np.testing.assert_array_equal(ref.assign_codes(x, q)[0], [0, 1, 2, 0, 3, 3, 0])
+
+
+def test_closed_form_degenerate_equal_steps():
+    """a = b: the two inner centres coincide at 0; codes 1/2 split at x <= 0 / x > 0."""
+    q = ref.closed_form_centers(np.array([0.5]), np.array([0.5]))
+    np.testing.assert_array_equal(q[0], [-1.0, 0.0, 0.0, 1.0])
+    codes = ref.assign_codes(np.array([[-0.1, 0.0, 0.1]]), q)
+    np.testing.assert_array_equal(codes[0], [1, 1, 2])
+
+
+# ----------------------------------------------------------------------------- packing (T14)
+@pytest.mark.parametrize("n", [1, 4, 7, 512, 771])
+def test_pack_roundtrip_and_size(n, rng):
+    codes = rng.integers(0, 4, size=(3, n)).astype(np.uint8)
+    packed = ref.pack2bit(codes)
+    assert packed.shape == (3, (n + 3) // 4)
+    np.testing.assert_array_equal(ref.unpack2bit(packed, n), codes)
+
+
+def test_pack_bit_order():
+    codes = np.array([[1, 2, 3, 0, 3]], dtype=np.uint8)
+    np.testing.assert_array_equal(ref.pack2bit(codes)[0], [1 | (2 << 2) | (3 << 4), 3])
+
+
+@pytest.mark.parametrize("n", [512, 4096, 11008])
+def test_bits_per_weight_closed_form(n):
+    """T14 (App. C): 2 + 2 code bits per weight plus two fp16 magnitudes per factor per column
+    gives 4 + 64/N bits per weight; the four-fp32-centres layout gives 4 + 256/N."""
+    m = 7
+    bits_fp16 = (2 * m * ((n + 3) // 4) * 8 + m * 2 * 2 * 16)
+    assert bits_fp16 / (m * n) == pytest.approx(4 + 64 / n) if n % 4 == 0 else True
+    bits_fp32 = (2 * m * ((n + 3) // 4) * 8 + m * 2 * 4 * 32)
+    assert bits_fp32 / (m * n) == pytest.approx(4 + 256 / n)
+
+
+def test_reconstruct_after_one_block_is_exact(rng):
+    """App. C reconstitution u_q + P v_q recovers u + P vhat when the factors are exactly
+    four-valued (one block, T8) -- so reconstruct = w - r."""
+    n = 32
+    eps = ref.sign_mask(n, 12)
+    w = rng.standard_normal((3, n))
+    pu, pv, centers, d = ref.quantize(w, eps, 1)
+    wh = ref.reconstruct(ref.unpack2bit(pu, n), ref.unpack2bit(pv, n), centers, eps)
+    np.testing.assert_allclose(wh, w - d["r"], atol=1e-13)
+
+
+# ----------------------------------------------------------------------------- replay
+def test_replay_with_own_signs_is_identity(rng):
+    n = 40
+    eps = ref.sign_mask(n, 13)
+    w = rng.standard_normal((3, n))
+    base = ref.decompose(w, eps, 3, trace=True)
+    rep = ref.decompose(w, eps, 3, replay_signs=base["trace"]["signs"], tau=1e-3)
+    np.testing.assert_array_equal(rep["u"], base["u"])
+    assert not rep["replay_outside"].any()
+    assert not rep["replay_in_band_flips"].any()
+
+
+def test_replay_flags_wrong_sign_outside_band(rng):
+    n = 40
+    eps = ref.sign_mask(n, 13)
+    w = rng.standard_normal((2, n))
+    base = ref.decompose(w, eps, 2, trace=True)
+    bad = base["trace"]["signs"].copy()
+    i = int(np.argmax(np.abs(w[0])))
+    bad[0, 0, i] = -bad[0, 0, i]
+    rep = ref.decompose(w, eps, 2, replay_signs=bad, tau=1e-9)
+    assert rep["replay_outside"][0] == 1 and rep["replay_outside"][1] == 0
