@@ -1,0 +1,134 @@
+/*
+ * kashin.h -- C ABI of the MI355X (gfx950) Kashin-DCT quantizer hot path.
+ *
+ * The method ("Structured Transforms for Low-Overhead Quantization of Language
+ * Models"): every weight vector w of length N (one row of an M x N matrix, one
+ * output channel) is decomposed by the Greedy Algorithm with Alternating Updates
+ * (Alg. 2) into w = u + P vhat + r, where P z = IDCT(eps * DCT(z)) is the
+ * orthonormal DCT-II conjugated by a Rademacher sign mask eps (Sec. 4.1), a
+ * symmetric involution (App. C).  Each factor is then quantised to 2-bit codes
+ * around four centres initialised in closed form at +-c1 +- c2 (Sec. 3.1) and
+ * packed four codes per byte (App. C).
+ *
+ * Conventions shared by every entry point
+ *   - Every function returns a status (KASHIN_OK or a negative KASHIN_E_*), never
+ *     throws, and records a message readable with kashin_last_error() (thread-local).
+ *   - All matrix pointers are DEVICE pointers owned by the caller.  The plan owns
+ *     only its own tables.  Matrices are row-major; row i of a matrix with leading
+ *     dimension ld starts at element i * ld.
+ *   - Arguments are validated on the host before anything is launched; invalid
+ *     arguments return KASHIN_E_INVALID / KASHIN_E_UNSUPPORTED_N and launch nothing.
+ *   - Launches are asynchronous on `stream` (a hipStream_t; NULL is the null
+ *     stream).  A failed launch returns KASHIN_E_HIP.  m == 0 is a no-op.
+ *   - Outputs are undefined after an error.  A row containing NaN or Inf yields NaN
+ *     factors, NaN centres and zero codes for that row only.
+ *   - Rows are processed two at a time (rows 2p and 2p+1 share one complex FFT).
+ *     Results are deterministic run to run; a row's last bits may depend on the
+ *     row it is paired with.
+ *   - Plans are immutable after creation and may be shared across host threads and
+ *     streams.  No entry point other than kashin_plan allocates device memory.
+ */
+#ifndef KASHIN_H_
+#define KASHIN_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kashin_plan_s* kashin_plan_t;
+
+enum {
+  KASHIN_OK = 0,
+  KASHIN_E_INVALID = -1,       /* null pointer, bad size, ld < N, iters < 1, dead plan, ... */
+  KASHIN_E_UNSUPPORTED_N = -2, /* vector length without a compiled kernel (see kashin_supported_n) */
+  KASHIN_E_NOMEM = -3,         /* host or device allocation failed (kashin_plan only) */
+  KASHIN_E_HIP = -4,           /* HIP runtime error (no device, launch failure, ...) */
+};
+
+enum { KASHIN_F32 = 0, KASHIN_F16 = 1 };
+
+/* 1 if vectors of length n have a compiled kernel, else 0.  Host only, no device needed. */
+int kashin_supported_n(int32_t n);
+
+/* The sign mask eps in {-1,+1}^n for `seed` (Sec. 4.1 T_E; Sec. 5 / App. C: one mask per
+ * layer drawn once from a fixed seed): eps_j = -1 iff the top bit of the j-th output of
+ * splitmix64 started at state `seed` is set.  Writes n int8 values to host memory `eps_host`.
+ * Host only, no device needed. */
+int kashin_signs(int32_t n, uint64_t seed, int8_t* eps_host);
+
+/* Create a plan for vectors of length n, sign mask from `sign_seed`, and `iters` blocks of
+ * Alg. 2 (each block = two u-steps and two vhat-steps).  Builds the FFT twiddle table and
+ * the eps-folded frequency table on the current HIP device (the only device allocation of
+ * this library).  Requires n even, kashin_supported_n(n), iters >= 1. */
+int kashin_plan(kashin_plan_t* out, int32_t n, uint64_t sign_seed, int32_t iters);
+
+/* Free a plan.  The caller must have synchronised every stream that used it. */
+int kashin_plan_destroy(kashin_plan_t plan);
+
+/* Copy the plan's n signs (+1/-1) to host memory. */
+int kashin_plan_signs(kashin_plan_t plan, int8_t* eps_host);
+
+/* Plan properties (host). */
+int kashin_plan_info(kashin_plan_t plan, int32_t* n, int32_t* iters, uint64_t* seed);
+
+/* Alg. 2 on every row of w (m x n, leading dimension ldw >= n, dtype KASHIN_F32 or
+ * KASHIN_F16; arithmetic is fp32).  Outputs, all fp32 row-major with leading dimension n:
+ *   u, vhat   m x n  factors with w = u + P vhat + r                       (required)
+ *   r         m x n  residual after the last block (costs one more P)      (nullable)
+ *   cstep     m x 4  magnitudes c of the four steps of block 0: c1, c2 (u-steps) and
+ *                    c3, c4 (vhat-steps), the closed-form centre inputs (Sec. 3.1) (nullable)
+ *   bounds    m x 4  ||u||_inf, ||vhat||_inf and the coefficient sums sum(c_u), sum(c_v)
+ *                    that bound them (App. F)                               (nullable) */
+int kashin_decompose(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw,
+                     float* u, float* vhat, float* r, float* cstep, float* bounds, void* stream);
+
+/* Four-peak 2-bit clustering of given factors (Sec. 3.1).  u, vhat: m x n fp32 (ld n);
+ * cstep: m x 4 from kashin_decompose.  Centres start at +-c1 +- c2 (u) and +-c3 +- c4
+ * (vhat), then `lloyd_iters` >= 0 plain 1-D k-means passes (an emptied cluster keeps its
+ * centre; centres re-sorted after each pass).  code = number of centre midpoints strictly
+ * below the value.  Outputs: codes_u, codes_v: m x ceil(n/4) bytes, code of element i in
+ * bits 2(i&3) of byte i>>2; centers: m x 2 x 4 fp32 ascending ([row][u=0|vhat=1][4]). */
+int kashin_cluster2bit(kashin_plan_t plan, const float* u, const float* vhat, const float* cstep,
+                       int64_t m, int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v,
+                       float* centers, void* stream);
+
+/* Load-time reconstitution w_hat = u_q + P v_q from codes and centres (App. C).
+ * w_hat: m x n fp32, leading dimension ldw >= n. */
+int kashin_reconstruct(kashin_plan_t plan, const uint8_t* codes_u, const uint8_t* codes_v,
+                       const float* centers, int64_t m, float* w_hat, int64_t ldw, void* stream);
+
+/* The fused hot path: kashin_decompose followed by kashin_cluster2bit without writing the
+ * factors: each row is read from HBM once and only codes and centres are written.
+ * Same layouts as kashin_decompose (input) and kashin_cluster2bit (outputs). */
+int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw,
+                    int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers,
+                    void* stream);
+
+/* y = P x row-wise for fp32 rows (m x n, ld n): the operator of Sec. 4.1 / Alg. 2 alone.
+ * x and y may not alias. */
+int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream);
+
+/* Test hook: replay record of Alg. 2 for selected rows.  For each of the `nrows` row
+ * indices in `rows` (device int64, each in [0, m)), the row is decomposed exactly as
+ * kashin_decompose does (paired with the same neighbour) and the kernel writes
+ *   sign_trace  nrows x 4k x n int8: sign (-1, 0, +1) taken at each atomic step, element
+ *               order of w (steps 4t, 4t+1 are u-steps, 4t+2, 4t+3 vhat-steps)
+ *   c_trace     nrows x 4k fp32: the step magnitudes c
+ *   u, vhat     nrows x n fp32 factors (ld n). */
+int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw,
+                 const int64_t* rows, int64_t nrows, int8_t* sign_trace, float* c_trace,
+                 float* u, float* vhat, void* stream);
+
+/* Static text for a status code. */
+const char* kashin_status_string(int status);
+
+/* Message of the last failed call on this host thread ("" if none). */
+const char* kashin_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KASHIN_H_ */

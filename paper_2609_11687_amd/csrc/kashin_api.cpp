@@ -1,0 +1,320 @@
+// C-ABI host layer: argument validation, plan construction (sign mask, FFT twiddles,
+// eps-folded frequency table) and kernel dispatch.  Every check runs on the host before
+// any HIP call, so argument errors are reported without touching a device.
+#include "kashin.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "kashin_internal.h"
+
+struct kashin_plan_s {
+  int32_t n = 0;
+  int32_t iters = 0;
+  uint64_t seed = 0;
+  int device = 0;
+  std::vector<int8_t> eps;
+  float2* d_tw = nullptr;   // exp(-2 pi i e / n), e in [0, n)
+  float2* d_mid = nullptr;  // eps-folded frequency factors
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+std::mutex g_plans_mu;
+std::set<const kashin_plan_s*> g_plans;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return KASHIN_OK;
+}
+
+bool live(const kashin_plan_s* p) {
+  std::lock_guard<std::mutex> lk(g_plans_mu);
+  return p != nullptr && g_plans.count(p) != 0;
+}
+
+// splitmix64 (Steele, Lea, Flood 2014): the eps generator, see kashin_signs.
+void make_signs(int32_t n, uint64_t seed, int8_t* out) {
+  uint64_t s = seed;
+  for (int32_t i = 0; i < n; ++i) {
+    s += 0x9E3779B97F4A7C15ull;
+    uint64_t z = s;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    out[i] = (z >> 63) ? int8_t(-1) : int8_t(1);
+  }
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(KASHIN_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int check_common(kashin_plan_t plan, int64_t m) {
+  if (!live(plan)) return fail(KASHIN_E_INVALID, "plan is null or destroyed");
+  if (m < 0) return fail(KASHIN_E_INVALID, "m must be >= 0 (got %lld)", (long long)m);
+  return KASHIN_OK;
+}
+
+kashin::KArgs base_args(const kashin_plan_s* p, int mode) {
+  kashin::KArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.tw = p->d_tw;
+  a.mid = p->d_mid;
+  a.iters = p->iters;
+  a.mode = mode;
+  return a;
+}
+
+int launch(const kashin_plan_s* p, const kashin::KArgs& a, int64_t grid, void* stream) {
+  const hipError_t e = kashin::launch_pair(p->n, a, grid, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int kashin_supported_n(int32_t n) { return (n >= 2 && (n % 2) == 0 && kashin::supported_n(n)) ? 1 : 0; }
+
+int kashin_signs(int32_t n, uint64_t seed, int8_t* eps_host) {
+  if (n < 1) return fail(KASHIN_E_INVALID, "n must be >= 1");
+  if (eps_host == nullptr) return fail(KASHIN_E_INVALID, "eps_host is null");
+  make_signs(n, seed, eps_host);
+  return ok();
+}
+
+int kashin_plan(kashin_plan_t* out, int32_t n, uint64_t sign_seed, int32_t iters) {
+  if (out == nullptr) return fail(KASHIN_E_INVALID, "out is null");
+  *out = nullptr;
+  if (iters < 1) return fail(KASHIN_E_INVALID, "iters must be >= 1 (got %d)", iters);
+  if (!kashin_supported_n(n)) return fail(KASHIN_E_UNSUPPORTED_N, "vector length %d has no compiled kernel", n);
+  kashin_plan_s* p = new (std::nothrow) kashin_plan_s();
+  if (p == nullptr) return fail(KASHIN_E_NOMEM, "host allocation failed");
+  p->n = n;
+  p->iters = iters;
+  p->seed = sign_seed;
+  p->eps.resize(n);
+  make_signs(n, sign_seed, p->eps.data());
+
+  // Host tables in double, rounded once to float.
+  std::vector<float2> tw(n), mid(n);
+  const double pi = 3.14159265358979323846;
+  for (int e = 0; e < n; ++e) {
+    const double ang = 2.0 * pi * double(e) / double(n);
+    tw[e] = make_float2(float(std::cos(ang)), float(-std::sin(ang)));
+  }
+  // Frequency factors: Y'_k = f_k Y_{s(k)}, with s(k) = k and f_k = eps_k / n when
+  // eps_k == eps_{n-k} (k = 0 and k = n/2 pair with themselves), else s(k) = n - k and
+  // f_k = eps_k exp(i pi k / n) / n (imaginary part never zero there).
+  for (int k = 0; k < n; ++k) {
+    const int partner = (n - k) % n;
+    const double ek = p->eps[k];
+    if (p->eps[k] == p->eps[partner]) {
+      mid[k] = make_float2(float(ek / n), 0.0f);
+    } else {
+      const double ang = pi * double(k) / double(n);
+      mid[k] = make_float2(float(ek * std::cos(ang) / n), float(ek * std::sin(ang) / n));
+    }
+  }
+  hipError_t e = hipGetDevice(&p->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->d_tw), sizeof(float2) * n);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->d_mid), sizeof(float2) * n);
+  if (e == hipSuccess) e = hipMemcpy(p->d_tw, tw.data(), sizeof(float2) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(p->d_mid, mid.data(), sizeof(float2) * n, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    if (p->d_tw) (void)hipFree(p->d_tw);
+    if (p->d_mid) (void)hipFree(p->d_mid);
+    delete p;
+    return hip_fail(e, "plan device tables");
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    g_plans.insert(p);
+  }
+  *out = p;
+  return ok();
+}
+
+int kashin_plan_destroy(kashin_plan_t plan) {
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    if (plan == nullptr || g_plans.erase(plan) == 0) return fail(KASHIN_E_INVALID, "plan is null or destroyed");
+  }
+  if (plan->d_tw) (void)hipFree(plan->d_tw);
+  if (plan->d_mid) (void)hipFree(plan->d_mid);
+  delete plan;
+  return ok();
+}
+
+int kashin_plan_signs(kashin_plan_t plan, int8_t* eps_host) {
+  if (!live(plan)) return fail(KASHIN_E_INVALID, "plan is null or destroyed");
+  if (eps_host == nullptr) return fail(KASHIN_E_INVALID, "eps_host is null");
+  std::memcpy(eps_host, plan->eps.data(), plan->eps.size());
+  return ok();
+}
+
+int kashin_plan_info(kashin_plan_t plan, int32_t* n, int32_t* iters, uint64_t* seed) {
+  if (!live(plan)) return fail(KASHIN_E_INVALID, "plan is null or destroyed");
+  if (n) *n = plan->n;
+  if (iters) *iters = plan->iters;
+  if (seed) *seed = plan->seed;
+  return ok();
+}
+
+int kashin_decompose(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw, float* u,
+                     float* vhat, float* r, float* cstep, float* bounds, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (m == 0) return ok();
+  if (!w || !u || !vhat) return fail(KASHIN_E_INVALID, "w, u and vhat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_DECOMPOSE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.u = u;
+  a.vhat = vhat;
+  a.r = r;
+  a.cstep = cstep;
+  a.bounds = bounds;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw, int32_t lloyd_iters,
+                    uint8_t* codes_u, uint8_t* codes_v, float* centers, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
+  if (m == 0) return ok();
+  if (!w || !codes_u || !codes_v || !centers) return fail(KASHIN_E_INVALID, "w, codes and centers must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_QUANTIZE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.lloyd = lloyd_iters;
+  a.codes_u = codes_u;
+  a.codes_v = codes_v;
+  a.centers = centers;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw, const int64_t* rows,
+                 int64_t nrows, int8_t* sign_trace, float* c_trace, float* u, float* vhat, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (nrows < 0) return fail(KASHIN_E_INVALID, "nrows must be >= 0");
+  if (nrows == 0 || m == 0) return ok();
+  if (!w || !rows || !sign_trace || !c_trace || !u || !vhat)
+    return fail(KASHIN_E_INVALID, "w, rows, sign_trace, c_trace, u and vhat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_TRACE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.rows = rows;
+  a.nrows = nrows;
+  a.tr_signs = sign_trace;
+  a.tr_c = c_trace;
+  a.u = u;
+  a.vhat = vhat;
+  return launch(plan, a, nrows, stream);
+}
+
+int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (m == 0) return ok();
+  if (!x || !y) return fail(KASHIN_E_INVALID, "x and y must be non-null");
+  if (x == y) return fail(KASHIN_E_INVALID, "x and y must not alias");
+  kashin::KArgs a = base_args(plan, kashin::MODE_APPLY_P);
+  a.w = x;
+  a.m = m;
+  a.ldw = plan->n;
+  a.y = y;
+  a.ldy = plan->n;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_reconstruct(kashin_plan_t plan, const uint8_t* codes_u, const uint8_t* codes_v, const float* centers,
+                       int64_t m, float* w_hat, int64_t ldw, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (m == 0) return ok();
+  if (!codes_u || !codes_v || !centers || !w_hat) return fail(KASHIN_E_INVALID, "codes, centers and w_hat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_RECON);
+  a.w = codes_u;
+  a.in_codes_v = codes_v;
+  a.in_centers = centers;
+  a.m = m;
+  a.y = w_hat;
+  a.ldy = ldw;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_cluster2bit(kashin_plan_t plan, const float* u, const float* vhat, const float* cstep, int64_t m,
+                       int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
+  if (m == 0) return ok();
+  if (!u || !vhat || !cstep || !codes_u || !codes_v || !centers)
+    return fail(KASHIN_E_INVALID, "u, vhat, cstep, codes and centers must be non-null");
+  kashin::ClusterArgs a;
+  a.u = u;
+  a.vhat = vhat;
+  a.cstep = cstep;
+  a.m = m;
+  a.n = plan->n;
+  a.lloyd = lloyd_iters;
+  a.codes_u = codes_u;
+  a.codes_v = codes_v;
+  a.centers = centers;
+  const hipError_t e = kashin::launch_cluster(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "cluster launch");
+  return ok();
+}
+
+const char* kashin_status_string(int status) {
+  switch (status) {
+    case KASHIN_OK: return "ok";
+    case KASHIN_E_INVALID: return "invalid argument";
+    case KASHIN_E_UNSUPPORTED_N: return "unsupported vector length";
+    case KASHIN_E_NOMEM: return "out of memory";
+    case KASHIN_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* kashin_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

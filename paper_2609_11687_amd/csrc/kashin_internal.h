@@ -1,0 +1,67 @@
+// Internal interface between the C-ABI host layer (kashin_api.cpp) and the HIP
+// kernels (kashin_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace kashin {
+
+enum Mode : int32_t {
+  MODE_DECOMPOSE = 0,  // write u, vhat (+ r, cstep, bounds)
+  MODE_QUANTIZE = 1,   // fused decompose + cluster + pack, write codes and centres only
+  MODE_TRACE = 2,      // decompose listed rows and record every sign decision
+  MODE_APPLY_P = 3,    // y = P x
+  MODE_RECON = 4,      // w_hat = u_q + P v_q
+};
+
+// Everything a launch needs, passed to the kernel by value.
+struct KArgs {
+  // operator tables (plan-owned, device)
+  const float2* tw;    // tw[e] = exp(-2 pi i e / N), e in [0, N)
+  const float2* mid;   // eps-folded frequency factors f_k; f_k.y != 0 marks a read from N - k
+  int32_t iters;       // blocks of Alg. 2
+  int32_t mode;
+  int32_t dtype;       // input dtype (KASHIN_F32 / KASHIN_F16)
+  int32_t lloyd;       // Lloyd passes for the fused clustering
+  int64_t m;           // rows in the matrix
+  int64_t ldw;         // leading dimension of the input matrix
+  const void* w;       // input rows (w, x, or codes_u for MODE_RECON)
+  // outputs / other inputs
+  float* u;
+  float* vhat;
+  float* r;
+  float* cstep;
+  float* bounds;
+  uint8_t* codes_u;
+  uint8_t* codes_v;
+  float* centers;
+  const uint8_t* in_codes_v;  // MODE_RECON
+  const float* in_centers;    // MODE_RECON
+  float* y;                   // MODE_APPLY_P / MODE_RECON output
+  int64_t ldy;
+  // trace
+  const int64_t* rows;
+  int64_t nrows;
+  int8_t* tr_signs;
+  float* tr_c;
+};
+
+struct ClusterArgs {
+  const float* u;
+  const float* vhat;
+  const float* cstep;
+  int64_t m;
+  int32_t n;
+  int32_t lloyd;
+  uint8_t* codes_u;
+  uint8_t* codes_v;
+  float* centers;
+};
+
+bool supported_n(int n);
+// Launch the pair kernel for vector length n; grid = number of work items (pairs or listed rows).
+hipError_t launch_pair(int n, const KArgs& a, int64_t grid, hipStream_t stream);
+hipError_t launch_cluster(const ClusterArgs& a, hipStream_t stream);
+
+}  // namespace kashin

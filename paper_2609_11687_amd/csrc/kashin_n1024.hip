@@ -1,0 +1,6 @@
+// Launch configuration for vectors of length 1024.
+#include "kashin_pair_impl.h"
+
+namespace kashin {
+KASHIN_DEFINE_SIZE(1024, 64, 16, 16, 4)
+}  // namespace kashin

@@ -1,0 +1,6 @@
+// Launch configuration for vectors of length 16384.
+#include "kashin_pair_impl.h"
+
+namespace kashin {
+KASHIN_DEFINE_SIZE(16384, 1024, 16, 16, 16, 4)
+}  // namespace kashin

@@ -1,0 +1,6 @@
+// Launch configuration for vectors of length 2048.
+#include "kashin_pair_impl.h"
+
+namespace kashin {
+KASHIN_DEFINE_SIZE(2048, 128, 16, 16, 8)
+}  // namespace kashin

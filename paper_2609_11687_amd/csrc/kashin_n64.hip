@@ -1,0 +1,6 @@
+// Launch configuration for vectors of length 64.
+#include "kashin_pair_impl.h"
+
+namespace kashin {
+KASHIN_DEFINE_SIZE(64, 64, 8, 8)
+}  // namespace kashin

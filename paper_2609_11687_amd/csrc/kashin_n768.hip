@@ -1,0 +1,6 @@
+// Launch configuration for vectors of length 768.
+#include "kashin_pair_impl.h"
+
+namespace kashin {
+KASHIN_DEFINE_SIZE(768, 64, 16, 16, 3)
+}  // namespace kashin

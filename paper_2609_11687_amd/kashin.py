@@ -1,0 +1,225 @@
+"""Thin ctypes binding of libkashin.so (argument marshalling only).
+
+Every function has the name of the C entry point it calls (see include/kashin.h)
+and takes torch tensors that already live on the GPU; all work runs in the HIP
+kernels.  A non-OK status raises ``KashinError`` carrying the library's message.
+There is no CPU fallback: if the library is not built, ``lib()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkashin.so")
+
+KASHIN_OK = 0
+KASHIN_E_INVALID = -1
+KASHIN_E_UNSUPPORTED_N = -2
+KASHIN_E_NOMEM = -3
+KASHIN_E_HIP = -4
+KASHIN_F32 = 0
+KASHIN_F16 = 1
+
+EXPORTS = (
+    "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
+    "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
+    "kashin_quantize", "kashin_apply_p", "kashin_trace", "kashin_status_string", "kashin_last_error",
+)
+
+_lib = None
+
+
+class KashinError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libkashin.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_11687_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    sig = {
+        "kashin_supported_n": [i32],
+        "kashin_signs": [i32, u64, vp],
+        "kashin_plan": [ctypes.POINTER(vp), i32, u64, i32],
+        "kashin_plan_destroy": [vp],
+        "kashin_plan_signs": [vp, vp],
+        "kashin_plan_info": [vp, vp, vp, vp],
+        "kashin_decompose": [vp, vp, i32, i64, i64, vp, vp, vp, vp, vp, vp],
+        "kashin_cluster2bit": [vp, vp, vp, vp, i64, i32, vp, vp, vp, vp],
+        "kashin_reconstruct": [vp, vp, vp, vp, i64, vp, i64, vp],
+        "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
+        "kashin_apply_p": [vp, vp, vp, i64, vp],
+        "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.kashin_status_string.argtypes = [ctypes.c_int]
+    L.kashin_status_string.restype = ctypes.c_char_p
+    L.kashin_last_error.argtypes = []
+    L.kashin_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != KASHIN_OK:
+        raise KashinError(status, lib().kashin_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return KASHIN_F32
+    if t.dtype == torch.float16:
+        return KASHIN_F16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _rows(w):
+    """(m, ldw) of a row-major 2-D tensor whose rows are unit-stride."""
+    if w.dim() != 2 or w.stride(1) != 1:
+        raise ValueError("expected a 2-D tensor with unit-stride rows")
+    return w.shape[0], w.stride(0)
+
+
+class Plan:
+    """Owns a kashin_plan_t; destroyed explicitly (``destroy``) or on garbage collection."""
+
+    def __init__(self, handle: ctypes.c_void_p, n: int, seed: int, iters: int):
+        self.handle = handle
+        self.n = n
+        self.seed = seed
+        self.iters = iters
+
+    def destroy(self) -> None:
+        if self.handle:
+            _check(lib().kashin_plan_destroy(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            if self.handle:
+                lib().kashin_plan_destroy(self.handle)
+        except Exception:
+            pass
+
+
+# ----------------------------------------------------------------------------- host-only
+def kashin_supported_n(n: int) -> bool:
+    return bool(lib().kashin_supported_n(n))
+
+
+def kashin_signs(n: int, seed: int):
+    import numpy as np
+    out = np.empty(n, dtype=np.int8)
+    _check(lib().kashin_signs(n, seed, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+# ----------------------------------------------------------------------------- plan
+def kashin_plan(n: int, seed: int, iters: int) -> Plan:
+    h = ctypes.c_void_p()
+    _check(lib().kashin_plan(ctypes.byref(h), n, seed, iters))
+    return Plan(h, n, seed, iters)
+
+
+def kashin_plan_destroy(plan: Plan) -> None:
+    plan.destroy()
+
+
+def kashin_plan_signs(plan: Plan):
+    import numpy as np
+    out = np.empty(plan.n, dtype=np.int8)
+    _check(lib().kashin_plan_signs(plan.handle, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def kashin_plan_info(plan: Plan):
+    n, it, sd = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_uint64()
+    _check(lib().kashin_plan_info(plan.handle, ctypes.byref(n), ctypes.byref(it), ctypes.byref(sd)))
+    return n.value, it.value, sd.value
+
+
+# ----------------------------------------------------------------------------- device calls
+def kashin_decompose(plan, w, u, vhat, r=None, cstep=None, bounds=None, stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_decompose(plan.handle, _ptr(w), _dtype_code(w), m, ldw, _ptr(u), _ptr(vhat), _ptr(r),
+                                  _ptr(cstep), _ptr(bounds), _stream(stream)))
+
+
+def kashin_cluster2bit(plan, u, vhat, cstep, lloyd_iters, codes_u, codes_v, centers, stream=None):
+    m = u.shape[0]
+    _check(lib().kashin_cluster2bit(plan.handle, _ptr(u), _ptr(vhat), _ptr(cstep), m, lloyd_iters, _ptr(codes_u),
+                                    _ptr(codes_v), _ptr(centers), _stream(stream)))
+
+
+def kashin_reconstruct(plan, codes_u, codes_v, centers, w_hat, stream=None):
+    m, ldw = _rows(w_hat)
+    _check(lib().kashin_reconstruct(plan.handle, _ptr(codes_u), _ptr(codes_v), _ptr(centers), m, _ptr(w_hat), ldw,
+                                    _stream(stream)))
+
+
+def kashin_quantize(plan, w, lloyd_iters, codes_u, codes_v, centers, stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_quantize(plan.handle, _ptr(w), _dtype_code(w), m, ldw, lloyd_iters, _ptr(codes_u),
+                                 _ptr(codes_v), _ptr(centers), _stream(stream)))
+
+
+def kashin_apply_p(plan, x, y, stream=None):
+    m = x.shape[0]
+    _check(lib().kashin_apply_p(plan.handle, _ptr(x), _ptr(y), m, _stream(stream)))
+
+
+def kashin_trace(plan, w, rows, sign_trace, c_trace, u, vhat, stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_trace(plan.handle, _ptr(w), _dtype_code(w), m, ldw, _ptr(rows), rows.numel(),
+                              _ptr(sign_trace), _ptr(c_trace), _ptr(u), _ptr(vhat), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- allocating helpers
+def quantize_alloc(plan, w, lloyd_iters=0, stream=None):
+    """Allocate outputs (torch, on w's device) and run kashin_quantize."""
+    import torch
+    m = w.shape[0]
+    nb = (plan.n + 3) // 4
+    cu = torch.empty((m, nb), dtype=torch.uint8, device=w.device)
+    cv = torch.empty((m, nb), dtype=torch.uint8, device=w.device)
+    ce = torch.empty((m, 2, 4), dtype=torch.float32, device=w.device)
+    kashin_quantize(plan, w, lloyd_iters, cu, cv, ce, stream)
+    return cu, cv, ce
+
+
+def decompose_alloc(plan, w, want_r=False, stream=None):
+    import torch
+    m, n = w.shape[0], plan.n
+    f = dict(dtype=torch.float32, device=w.device)
+    u = torch.empty((m, n), **f)
+    vh = torch.empty((m, n), **f)
+    r = torch.empty((m, n), **f) if want_r else None
+    cs = torch.empty((m, 4), **f)
+    bd = torch.empty((m, 4), **f)
+    kashin_decompose(plan, w, u, vh, r, cs, bd, stream)
+    return u, vh, r, cs, bd

@@ -1,0 +1,91 @@
+"""Host-only checks of the C-ABI library: it loads, exports every declared entry point,
+computes the sign mask like the oracle, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle.kashin_ref as ref
+from paper_2609_11687_amd import kashin as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kashin.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kashin_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = K.lib()
+    names = _declared()
+    assert len(names) >= 13
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(K.EXPORTS)
+
+
+@pytest.mark.parametrize("n", [64, 96, 172, 512, 768, 1024, 3072, 4096, 11008, 16384])
+def test_supported_sizes(n):
+    assert K.kashin_supported_n(n)
+
+
+@pytest.mark.parametrize("n", [0, 1, 2, 7, 100, 4095, 4097, 32768])
+def test_unsupported_sizes(n):
+    assert not K.kashin_supported_n(n)
+
+
+@pytest.mark.parametrize("n,seed", [(64, 0), (512, 1), (4096, 123456789), (11008, 2**64 - 1)])
+def test_signs_match_oracle(n, seed):
+    np.testing.assert_array_equal(K.kashin_signs(n, seed), ref.sign_mask(n, seed))
+
+
+def test_signs_published_top_bits():
+    # splitmix64 from state 0 starts 0xe220..., 0x6e78..., 0x06c4...: top bits 1, 0, 0
+    np.testing.assert_array_equal(K.kashin_signs(3, 0), [-1, 1, 1])
+
+
+def test_plan_validation_before_device():
+    L = K.lib()
+    h = ctypes.c_void_p()
+    assert L.kashin_plan(None, 512, 0, 20) == K.KASHIN_E_INVALID
+    assert L.kashin_plan(ctypes.byref(h), 512, 0, 0) == K.KASHIN_E_INVALID
+    assert "iters" in L.kashin_last_error().decode()
+    assert L.kashin_plan(ctypes.byref(h), 511, 0, 20) == K.KASHIN_E_UNSUPPORTED_N
+    assert L.kashin_plan(ctypes.byref(h), 100, 0, 20) == K.KASHIN_E_UNSUPPORTED_N
+    assert not h.value
+
+
+def test_calls_reject_dead_plan():
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1234)
+    buf = ctypes.c_void_p(0x1000)
+    assert L.kashin_decompose(None, buf, 0, 4, 512, buf, buf, None, None, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_decompose(fake, buf, 0, 4, 512, buf, buf, None, None, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize(fake, buf, 0, 4, 512, 0, buf, buf, buf, None) == K.KASHIN_E_INVALID
+    assert L.kashin_apply_p(None, buf, buf, 4, None) == K.KASHIN_E_INVALID
+    assert L.kashin_plan_destroy(fake) == K.KASHIN_E_INVALID
+    assert L.kashin_plan_signs(None, buf) == K.KASHIN_E_INVALID
+    assert "plan" in L.kashin_last_error().decode()
+
+
+def test_status_strings():
+    L = K.lib()
+    for st in (0, -1, -2, -3, -4):
+        assert L.kashin_status_string(st)
+    assert L.kashin_status_string(0) == b"ok"
+
+
+def test_plan_needs_a_device_or_succeeds():
+    """With no GPU the plan's table upload fails with KASHIN_E_HIP (after host validation)."""
+    L = K.lib()
+    h = ctypes.c_void_p()
+    st = L.kashin_plan(ctypes.byref(h), 512, 0, 20)
+    if st == K.KASHIN_OK:
+        assert L.kashin_plan_destroy(h) == K.KASHIN_OK
+    else:
+        assert st == K.KASHIN_E_HIP

@@ -1,0 +1,330 @@
+"""GPU parity of the HIP path (called through the C ABI) against the float64 oracle.
+
+See parity_util for the tolerances and the tie-band replay.  Inputs are seeded and
+synthetic (paper_2609_11687_amd.synth); every size spans several FFT tiles, and the
+odd row counts exercise the unpaired last row.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.kashin_ref as ref
+from paper_2609_11687_amd import kashin as K
+from paper_2609_11687_amd import synth
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+ALL_N = [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 8192, 11008, 16384]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    K.lib()
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _rows(rng, m, n, dist="gauss", std=0.02):
+    if dist == "gauss":
+        w = rng.standard_normal((m, n)) * std
+    elif dist == "t4":
+        w = rng.standard_t(4, (m, n)) * (std / np.sqrt(2.0))
+    elif dist == "outlier":
+        w = rng.standard_normal((m, n)) * std
+        w[:, rng.choice(n, max(1, n // 1000), replace=False)] *= 20.0
+    else:
+        raise ValueError(dist)
+    return w.astype(np.float32)
+
+
+# ----------------------------------------------------------------------------- operator P
+@pytest.mark.parametrize("n", ALL_N)
+def test_apply_p_matches_oracle(n):
+    rng = np.random.default_rng(n)
+    seed = 1000 + n
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, 1)
+    np.testing.assert_array_equal(K.kashin_plan_signs(plan), eps)
+    x = rng.standard_normal((5, n)).astype(np.float32)
+    xd = pu.to_dev(x)
+    y = torch.empty_like(xd)
+    K.kashin_apply_p(plan, xd, y)
+    y2 = torch.empty_like(xd)
+    K.kashin_apply_p(plan, y, y2)
+    torch.cuda.synchronize()
+    yref = ref.apply_p(x.astype(np.float64), eps)
+    scale = max(np.abs(x).max(), np.abs(yref).max())
+    err = np.abs(y.cpu().numpy() - yref).max() / scale
+    _say(f"apply_p N={n}: max err / scale = {err:.2e}")
+    assert err <= 5e-6
+    # involution: P(P x) = x
+    assert np.abs(y2.cpu().numpy() - x).max() / scale <= 1e-5
+
+
+# ----------------------------------------------------------------------------- Alg. 2 on small batches
+CASES = [(64, 3, "gauss"), (96, 20, "gauss"), (172, 20, "t4"), (256, 1, "gauss"), (512, 20, "gauss"),
+         (768, 30, "outlier"), (1024, 8, "t4"), (2048, 20, "gauss"), (3072, 30, "outlier"), (4096, 30, "t4")]
+
+
+@pytest.mark.parametrize("n,k,dist", CASES)
+def test_decompose_replay_parity(n, k, dist):
+    rng = np.random.default_rng(7 * n + k)
+    m = 7
+    w = _rows(rng, m, n, dist)
+    seed = 17 + n
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, k)
+    wd = pu.to_dev(w)
+    u, vh, r, cs, bd = K.decompose_alloc(plan, wd, want_r=True)
+    signs, c_tr, u_tr, v_tr = pu.gpu_trace(plan, wd, list(range(m)), k)
+    u, vh, r, cs, bd = (t.cpu().numpy() for t in (u, vh, r, cs, bd))
+    # the trace run is the same computation as decompose: identical bits
+    np.testing.assert_array_equal(u_tr, u.astype(np.float64))
+    np.testing.assert_array_equal(v_tr, vh.astype(np.float64))
+    w64 = w.astype(np.float64)
+    res = pu.replay_parity(w64, eps, k, signs, u.astype(np.float64), vh.astype(np.float64))
+    _say(f"decompose N={n} k={k} {dist}: du={res['du'].max():.2e} dv={res['dv'].max():.2e} "
+         f"rec={res['rec'].max():.2e} in-band flips={res['in_band_flips'].sum()} direct ok={res['direct_frac_ok']:.2f}")
+    pu.assert_replay_ok(res, f"N={n}")
+    rep = res["rep"]
+    winf = res["winf"]
+    # step magnitudes: block-0 c's and the whole c trace agree with the replayed oracle
+    np.testing.assert_allclose(cs, rep["cstep"], rtol=1e-5, atol=1e-7 * winf.max())
+    # factor bounds: max norms of the returned factors, coefficient sums of App. F
+    np.testing.assert_allclose(bd[:, 0], np.abs(u).max(axis=1), rtol=1e-6)
+    np.testing.assert_allclose(bd[:, 1], np.abs(vh).max(axis=1), rtol=1e-6)
+    np.testing.assert_allclose(bd[:, 2], rep["csum"][:, 0], rtol=1e-5)
+    np.testing.assert_allclose(bd[:, 3], rep["csum"][:, 1], rtol=1e-5)
+    assert np.all(bd[:, 0] <= bd[:, 2] * (1 + 1e-5)) and np.all(bd[:, 1] <= bd[:, 3] * (1 + 1e-5))
+    # residual output: w = u + P vhat + r
+    rec = np.abs(w64 - u - ref.apply_p(vh.astype(np.float64), eps) - r).max(axis=1) / winf
+    assert rec.max() <= 1e-5
+
+
+# ----------------------------------------------------------------------------- clustering and packing
+@pytest.mark.parametrize("n,k,lloyd", [(512, 20, 0), (768, 30, 0), (512, 20, 2), (4096, 30, 0), (96, 5, 3)])
+def test_quantize_codes_and_reconstruct(n, k, lloyd):
+    rng = np.random.default_rng(n + 100 * lloyd)
+    m = 9
+    w = _rows(rng, m, n, "t4")
+    seed = 5 + n
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, k)
+    wd = pu.to_dev(w)
+    cu, cv, ce = K.quantize_alloc(plan, wd, lloyd)
+    u, vh, _, cs, _ = K.decompose_alloc(plan, wd)
+    nb = (n + 3) // 4
+    cu2 = torch.empty((m, nb), dtype=torch.uint8, device="cuda")
+    cv2 = torch.empty_like(cu2)
+    ce2 = torch.empty((m, 2, 4), dtype=torch.float32, device="cuda")
+    K.kashin_cluster2bit(plan, u, vh, cs, lloyd, cu2, cv2, ce2)
+    what = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    K.kashin_reconstruct(plan, cu, cv, ce, what)
+    torch.cuda.synchronize()
+    cu, cv, ce = cu.cpu().numpy(), cv.cpu().numpy(), ce.cpu().numpy().astype(np.float64)
+    u64, v64, cs64 = (t.cpu().numpy().astype(np.float64) for t in (u, vh, cs))
+    winf = np.abs(w).max(axis=1).astype(np.float64)
+    codes_u, codes_v = pu.unpack(cu, n), pu.unpack(cv, n)
+    # (1) fused clustering == standalone clustering of the same factors
+    if lloyd == 0:
+        np.testing.assert_array_equal(cu, cu2.cpu().numpy())
+        np.testing.assert_array_equal(cv, cv2.cpu().numpy())
+        np.testing.assert_array_equal(ce, ce2.cpu().numpy())
+    # (2) centres: closed form from the oracle's c's then Lloyd, and codes, vs the oracle
+    qu = ref.closed_form_centers(cs64[:, 0], cs64[:, 1])
+    qv = ref.closed_form_centers(cs64[:, 2], cs64[:, 3])
+    if lloyd:
+        qu = ref.lloyd(u64, qu, lloyd)
+        qv = ref.lloyd(v64, qv, lloyd)
+    np.testing.assert_allclose(ce[:, 0], qu, rtol=0, atol=1e-5 * winf.max())
+    np.testing.assert_allclose(ce[:, 1], qv, rtol=0, atol=1e-5 * winf.max())
+    mu, tot = pu.code_mismatches(codes_u, u64, qu, winf, "u")
+    mv, _ = pu.code_mismatches(codes_v, v64, qv, winf, "vhat")
+    _say(f"quantize N={n} lloyd={lloyd}: code mismatches u={mu} v={mv} of {tot}")
+    assert mu + mv <= max(1, int(1e-4 * 2 * tot))
+    # (3) reconstruction from codes == the oracle's dequantisation of the same codes
+    wref = ref.reconstruct(codes_u, codes_v, ce, eps)
+    err = np.abs(what.cpu().numpy() - wref).max(axis=1) / winf
+    assert err.max() <= 1e-5
+    # packing layout: bytes decode to in-range codes and the padded tail is zero
+    if n % 4:
+        assert not (cu[:, -1] >> (2 * (n % 4))).any()
+
+
+def test_codes_against_oracle_decomposition():
+    """Codes of the fused path versus codes the oracle derives from its own (replayed)
+    decomposition, closed-form centres, decisions in fp32."""
+    n, k, m = 1024, 20, 11
+    rng = np.random.default_rng(99)
+    w = _rows(rng, m, n, "t4")
+    eps = ref.sign_mask(n, 21)
+    plan = K.kashin_plan(n, 21, k)
+    wd = pu.to_dev(w)
+    cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, list(range(m)), k)
+    w64 = w.astype(np.float64)
+    res = pu.replay_parity(w64, eps, k, signs, u_tr, v_tr)
+    pu.assert_replay_ok(res)
+    rep = res["rep"]
+    qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
+    qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+    np.testing.assert_allclose(ce.cpu().numpy()[:, 0], qu, rtol=1e-5, atol=0)
+    np.testing.assert_allclose(ce.cpu().numpy()[:, 1], qv, rtol=1e-5, atol=0)
+    mu, tot = pu.code_mismatches(pu.unpack(cu.cpu().numpy(), n), rep["u"], qu, res["winf"], "u")
+    mv, _ = pu.code_mismatches(pu.unpack(cv.cpu().numpy(), n), rep["vhat"], qv, res["winf"], "vhat")
+    assert mu + mv <= max(1, int(2e-4 * tot))
+
+
+# ----------------------------------------------------------------------------- properties and edges
+def test_deterministic_and_pow2_homogeneous():
+    n, k, m = 512, 20, 6
+    rng = np.random.default_rng(3)
+    w = _rows(rng, m, n)
+    plan = K.kashin_plan(n, 9, k)
+    out1 = K.decompose_alloc(plan, pu.to_dev(w))
+    out2 = K.decompose_alloc(plan, pu.to_dev(w))
+    out4 = K.decompose_alloc(plan, pu.to_dev(w * 4.0))
+    outn = K.decompose_alloc(plan, pu.to_dev(-w))
+    torch.cuda.synchronize()
+    for i in (0, 1):
+        a = out1[i].cpu().numpy()
+        np.testing.assert_array_equal(a, out2[i].cpu().numpy())
+        np.testing.assert_array_equal(4.0 * a, out4[i].cpu().numpy())
+        np.testing.assert_array_equal(-a, outn[i].cpu().numpy())
+
+
+def test_fp16_input_equals_fp32_of_same_values():
+    n, k, m = 4096, 10, 4
+    rng = np.random.default_rng(4)
+    w16 = _rows(rng, m, n).astype(np.float16)
+    plan = K.kashin_plan(n, 2, k)
+    a = K.decompose_alloc(plan, pu.to_dev(w16))
+    b = K.decompose_alloc(plan, pu.to_dev(w16.astype(np.float32)))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(a[0].cpu().numpy(), b[0].cpu().numpy())
+    np.testing.assert_array_equal(a[1].cpu().numpy(), b[1].cpu().numpy())
+
+
+def test_empty_single_and_strided_rows():
+    n, k = 256, 5
+    plan = K.kashin_plan(n, 1, k)
+    rng = np.random.default_rng(5)
+    # m = 0: no-op
+    w0 = torch.empty((0, n), dtype=torch.float32, device="cuda")
+    K.kashin_decompose(plan, w0, w0, w0)
+    # m = 1 (unpaired row) and a strided view (ldw = n + 40)
+    wide = _rows(rng, 3, n + 40)
+    wv = pu.to_dev(wide)[:, 5:5 + n]
+    assert wv.stride(0) == n + 40
+    u, vh, _, _, _ = K.decompose_alloc(plan, wv)
+    u1, vh1, _, _, _ = K.decompose_alloc(plan, pu.to_dev(wide[2:3, 5:5 + n]))
+    torch.cuda.synchronize()
+    eps = ref.sign_mask(n, 1)
+    w64 = wide[:, 5:5 + n].astype(np.float64)
+    rec = np.abs(w64 - u.cpu().numpy() - ref.apply_p(vh.cpu().numpy().astype(np.float64), eps)).max(1)
+    assert rec.max() <= 1e-5 * np.abs(w64).max()
+    # the unpaired last row of the 3-row call equals the 1-row call bit for bit
+    np.testing.assert_array_equal(u.cpu().numpy()[2], u1.cpu().numpy()[0])
+
+
+def test_nonfinite_row_is_isolated():
+    n, k, m = 512, 10, 4
+    rng = np.random.default_rng(6)
+    w = _rows(rng, m, n)
+    w_bad = w.copy()
+    w_bad[2, 17] = np.nan
+    w_bad[1, 3] = np.inf
+    plan = K.kashin_plan(n, 4, k)
+    u, vh, _, cs, _ = K.decompose_alloc(plan, pu.to_dev(w_bad))
+    cu, cv, ce = K.quantize_alloc(plan, pu.to_dev(w_bad))
+    torch.cuda.synchronize()
+    u, vh, ce = u.cpu().numpy(), vh.cpu().numpy(), ce.cpu().numpy()
+    assert np.isnan(u[2]).all() and np.isnan(vh[2]).all() and np.isnan(u[1]).all()
+    assert np.isnan(ce[1]).all() and np.isnan(ce[2]).all()
+    assert not cu.cpu().numpy()[1:3].any()
+    # partners (rows 0 and 3) are finite and still decompose their own rows
+    eps = ref.sign_mask(n, 4)
+    for row in (0, 3):
+        assert np.isfinite(u[row]).all()
+        rec = np.abs(w[row] - u[row] - ref.apply_p(vh[row:row + 1].astype(np.float64), eps)[0]).max()
+        assert rec <= 1e-5 * np.abs(w[row]).max()
+
+
+def test_zero_and_cube_vertex_rows():
+    """A zero row stays zero; a row a*s (s in {-1,1}^N) is all u after one step (T11)."""
+    n, k = 512, 4
+    s = np.where(np.arange(n) % 3 == 0, -1.0, 1.0).astype(np.float32)
+    w = np.stack([np.zeros(n, np.float32), 0.75 * s, 0.25 * s, np.zeros(n, np.float32)])
+    plan = K.kashin_plan(n, 8, k)
+    u, vh, _, cs, _ = K.decompose_alloc(plan, pu.to_dev(w))
+    torch.cuda.synchronize()
+    u, vh, cs = u.cpu().numpy(), vh.cpu().numpy(), cs.cpu().numpy()
+    assert not u[0].any() and not vh[0].any() and not u[3].any()
+    np.testing.assert_allclose(u[1], w[1], atol=1e-6)
+    assert np.abs(vh[1]).max() <= 1e-6
+    np.testing.assert_allclose(cs[1], [0.75, 0, 0, 0], atol=1e-7)
+
+
+# ----------------------------------------------------------------------------- full-size workloads, sampled rows
+def _sample_rows(w, count, rng):
+    m = w.shape[0]
+    pick = {0, m - 1, int(np.argmax(np.abs(w.astype(np.float32)).max(axis=1)))}
+    while len(pick) < min(count, m):
+        pick.add(int(rng.integers(0, m)))
+    return sorted(pick)
+
+
+WL = [("gauss512", None), ("opt125m", 4), ("llama7b", 3), ("pythia7b", 2)]
+
+
+@pytest.mark.parametrize("key,per_matrix", WL)
+def test_workload_sampled_rows(key, per_matrix):
+    """Every matrix of the workload quantised in full (the launch configuration the benchmark
+    times); sampled rows replayed against the oracle (factors, reconstruction, codes)."""
+    wl = synth.WORKLOADS[key]
+    rng = np.random.default_rng(11)
+    total_m = total_codes = 0
+    for idx, spec in enumerate(wl.matrices):
+        if key == "llama7b" and spec.name in ("k_proj", "v_proj", "up_proj"):
+            continue  # same shapes as q_proj / gate_proj; keeps the test within its time budget
+        if key == "pythia7b" and spec.name in ("qkv_1", "qkv_2", "dense"):
+            continue
+        w = synth.make_matrix(wl, 0, idx)
+        seed = synth.sign_seed(wl, 0, idx)
+        plan = K.kashin_plan(spec.n, seed, wl.iters)
+        dt = torch.float16 if spec.dtype == "f16" else torch.float32
+        wd = pu.to_dev(w).to(dt)
+        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+        rows = list(range(w.shape[0])) if per_matrix is None else _sample_rows(w, per_matrix, rng)
+        signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, rows, wl.iters)
+        eps = ref.sign_mask(spec.n, seed)
+        w64 = w[rows].astype(np.float64)
+        res = pu.replay_parity(w64, eps, wl.iters, signs, u_tr, v_tr)
+        _say(f"{key}/{spec.name} N={spec.n} rows={len(rows)}: du={res['du'].max():.2e} "
+             f"dv={res['dv'].max():.2e} rec={res['rec'].max():.2e} direct ok={res['direct_frac_ok']:.2f}")
+        pu.assert_replay_ok(res, f"{key}/{spec.name}")
+        rep = res["rep"]
+        qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
+        qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+        ce_s = ce.cpu().numpy()[rows]
+        np.testing.assert_allclose(ce_s[:, 0], qu, rtol=1e-5)
+        np.testing.assert_allclose(ce_s[:, 1], qv, rtol=1e-5)
+        codes_u = pu.unpack(cu.cpu().numpy()[rows], spec.n)
+        codes_v = pu.unpack(cv.cpu().numpy()[rows], spec.n)
+        mu, tot = pu.code_mismatches(codes_u, rep["u"], qu, res["winf"], "u")
+        mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat")
+        total_m += mu + mv
+        total_codes += 2 * tot
+        # every row of the matrix got finite centres
+        assert np.isfinite(ce.cpu().numpy()).all()
+        del plan
+    _say(f"{key}: code mismatches {total_m} of {total_codes}")
+    assert total_m <= max(1, int(1e-4 * total_codes))
