@@ -80,7 +80,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--lloyd", type=int, default=0)
-    ap.add_argument("--cpu-rows", type=int, default=6)
+    ap.add_argument("--cpu-rows", type=int, default=256)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))

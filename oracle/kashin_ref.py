@@ -158,7 +158,8 @@ def decompose(w, eps, k, *, replay_signs=None, tau=None, trace=False):
 
     Replay (a validity check of another implementation's choices at near-ties,
     used by the GPU parity tests): with ``replay_signs`` (B, 4k, n) int8 and
-    ``tau`` (B,), at atomic step s of row b, while that step's c >= tau[b], every
+    ``tau`` (B,), at atomic step s of row b, while that step's c >= tau[b] >= 0 (a
+    negative tau switches replay off for that row), every
     entry whose float64 value satisfies |x_i| <= tau[b] takes the sign given in
     ``replay_signs[b, s, i]`` instead of sign(x_i).  All other decisions and all
     arithmetic stay float64 and the oracle's own.  ``out['replay_outside']``
@@ -203,7 +204,7 @@ def decompose(w, eps, k, *, replay_signs=None, tau=None, trace=False):
         s = np.sign(x)
         if replay_signs is not None:
             gs = replay_signs[:, step, :].astype(np.float64)
-            live = (c >= tau)[:, None]
+            live = ((c >= tau) & (tau >= 0))[:, None]
             band = live & (np.abs(x) <= tau[:, None])
             wrong = live & ~band & (gs != s)
             outside[:] += wrong.sum(axis=1)

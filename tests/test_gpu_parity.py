@@ -104,9 +104,10 @@ def test_decompose_replay_parity(n, k, dist):
     np.testing.assert_allclose(bd[:, 2], rep["csum"][:, 0], rtol=1e-5)
     np.testing.assert_allclose(bd[:, 3], rep["csum"][:, 1], rtol=1e-5)
     assert np.all(bd[:, 0] <= bd[:, 2] * (1 + 1e-5)) and np.all(bd[:, 1] <= bd[:, 3] * (1 + 1e-5))
-    # residual output: w = u + P vhat + r
+    # residual output: w = u + P vhat + r, and r itself against the oracle's residual
     rec = np.abs(w64 - u - ref.apply_p(vh.astype(np.float64), eps) - r).max(axis=1) / winf
     assert rec.max() <= 1e-5
+    assert (np.abs(r - rep["r"]).max(axis=1) / winf).max() <= 1e-5
 
 
 # ----------------------------------------------------------------------------- clustering and packing
@@ -229,7 +230,8 @@ def test_empty_single_and_strided_rows():
     torch.cuda.synchronize()
     eps = ref.sign_mask(n, 1)
     w64 = wide[:, 5:5 + n].astype(np.float64)
-    rec = np.abs(w64 - u.cpu().numpy() - ref.apply_p(vh.cpu().numpy().astype(np.float64), eps)).max(1)
+    r_ref = ref.decompose(w64, eps, k)["r"]  # k = 5 leaves a residual above fp32 resolution
+    rec = np.abs(w64 - r_ref - u.cpu().numpy() - ref.apply_p(vh.cpu().numpy().astype(np.float64), eps)).max(1)
     assert rec.max() <= 1e-5 * np.abs(w64).max()
     # the unpaired last row of the 3-row call equals the 1-row call bit for bit
     np.testing.assert_array_equal(u.cpu().numpy()[2], u1.cpu().numpy()[0])

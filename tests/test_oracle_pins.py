@@ -383,3 +383,14 @@ def test_replay_flags_wrong_sign_outside_band(rng):
     bad[0, 0, i] = -bad[0, 0, i]
     rep = ref.decompose(w, eps, 2, replay_signs=bad, tau=1e-9)
     assert rep["replay_outside"][0] == 1 and rep["replay_outside"][1] == 0
+
+
+def test_replay_negative_tau_is_plain_run(rng):
+    n = 40
+    eps = ref.sign_mask(n, 13)
+    w = rng.standard_normal((2, n))
+    base = ref.decompose(w, eps, 2, trace=True)
+    junk = np.ones_like(base["trace"]["signs"])
+    rep = ref.decompose(w, eps, 2, replay_signs=junk, tau=np.array([-1.0, -1.0]))
+    np.testing.assert_array_equal(rep["u"], base["u"])
+    assert not rep["replay_outside"].any()
