@@ -23,8 +23,9 @@ struct kashin_plan_s {
   uint64_t seed = 0;
   int device = 0;
   std::vector<int8_t> eps;
-  float2* d_tw = nullptr;   // exp(-2 pi i e / n), e in [0, n)
-  float2* d_mid = nullptr;  // eps-folded frequency factors
+  void* d_tables = nullptr;  // twiddle tables, then the eps table (16-byte aligned)
+  float2* d_tw = nullptr;
+  float4* d_mid = nullptr;
 };
 
 namespace {
@@ -66,6 +67,65 @@ void make_signs(int32_t n, uint64_t seed, int8_t* out) {
   }
 }
 
+int pad_slot(int i) { return i + (i >> 4); }  // LDS slot of element i (kernel layout)
+
+// Tables of the pair kernel for length n (layout shared with kashin_pair_impl.h):
+//  tw:  one table per Stockham pass with stride NS > 1 -- forward passes 1..np-1, then
+//       inverse passes 1..np-1 (radices in reverse order) -- entry [jm][r] =
+//       exp(-2 pi i r jm / (NS R)), each table padded to an even length;
+//  mid: for the first inverse pass (radix R = last forward radix, stride 1), entry j R + r
+//       for element k = j + r n/R: Y'_k = f_k Y_s(k) with s(k) = k and f_k = eps_k / n when
+//       eps_k == eps_{n-k} (k = 0 and k = n/2 pair with themselves), else s(k) = n - k and
+//       f_k = eps_k exp(i pi k / n) / n; stored as {Re f, Im f, LDS byte address of s(k), 0}.
+void build_tables(int n, const int8_t* eps, std::vector<float2>* tw, std::vector<float4>* mid) {
+  kashin::PlanShape sh;
+  kashin::plan_shape(n, &sh);
+  const double pi = 3.14159265358979323846;
+  auto add_table = [&](int R, int NS) {
+    for (int jm = 0; jm < NS; ++jm)
+      for (int r = 0; r < R; ++r) {
+        const double ang = -2.0 * pi * double(r) * double(jm) / (double(NS) * double(R));
+        tw->push_back(make_float2(float(std::cos(ang)), float(std::sin(ang))));
+      }
+    if (tw->size() % 2) tw->push_back(make_float2(0.f, 0.f));
+  };
+  for (int q = 1; q < sh.np; ++q) {  // forward passes
+    int ns = 1;
+    for (int i = 0; i < q; ++i) ns *= sh.rad[i];
+    add_table(sh.rad[q], ns);
+  }
+  for (int q = 1; q < sh.np; ++q) {  // inverse passes
+    int ns = 1;
+    for (int i = 0; i < q; ++i) ns *= sh.rad[sh.np - 1 - i];
+    add_table(sh.rad[sh.np - 1 - q], ns);
+  }
+  const int R = sh.rad[sh.np - 1];
+  const int nb = n / R;
+  mid->assign(n, make_float4(0.f, 0.f, 0.f, 0.f));
+  for (int j = 0; j < nb; ++j)
+    for (int r = 0; r < R; ++r) {
+      const int k = j + r * nb;
+      const int partner = (n - k) % n;
+      const double ek = eps[k];
+      float fx, fy;
+      int src;
+      if (eps[k] == eps[partner]) {
+        fx = float(ek / n);
+        fy = 0.f;
+        src = k;
+      } else {
+        const double ang = pi * double(k) / double(n);
+        fx = float(ek * std::cos(ang) / n);
+        fy = float(ek * std::sin(ang) / n);
+        src = partner;
+      }
+      const int addr = pad_slot(src) * int(sizeof(float2));
+      float faddr;
+      std::memcpy(&faddr, &addr, sizeof(faddr));
+      (*mid)[j * R + r] = make_float4(fx, fy, faddr, 0.f);
+    }
+}
+
 int hip_fail(hipError_t e, const char* what) {
   return fail(KASHIN_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -80,7 +140,7 @@ kashin::KArgs base_args(const kashin_plan_s* p, int mode) {
   kashin::KArgs a;
   std::memset(&a, 0, sizeof(a));
   a.tw = p->d_tw;
-  a.mid = p->d_mid;
+  a.mid4 = p->d_mid;
   a.iters = p->iters;
   a.mode = mode;
   return a;
@@ -118,34 +178,21 @@ int kashin_plan(kashin_plan_t* out, int32_t n, uint64_t sign_seed, int32_t iters
   p->eps.resize(n);
   make_signs(n, sign_seed, p->eps.data());
 
-  // Host tables in double, rounded once to float.
-  std::vector<float2> tw(n), mid(n);
-  const double pi = 3.14159265358979323846;
-  for (int e = 0; e < n; ++e) {
-    const double ang = 2.0 * pi * double(e) / double(n);
-    tw[e] = make_float2(float(std::cos(ang)), float(-std::sin(ang)));
-  }
-  // Frequency factors: Y'_k = f_k Y_{s(k)}, with s(k) = k and f_k = eps_k / n when
-  // eps_k == eps_{n-k} (k = 0 and k = n/2 pair with themselves), else s(k) = n - k and
-  // f_k = eps_k exp(i pi k / n) / n (imaginary part never zero there).
-  for (int k = 0; k < n; ++k) {
-    const int partner = (n - k) % n;
-    const double ek = p->eps[k];
-    if (p->eps[k] == p->eps[partner]) {
-      mid[k] = make_float2(float(ek / n), 0.0f);
-    } else {
-      const double ang = pi * double(k) / double(n);
-      mid[k] = make_float2(float(ek * std::cos(ang) / n), float(ek * std::sin(ang) / n));
-    }
-  }
+  std::vector<float2> tw;
+  std::vector<float4> mid;
+  build_tables(n, p->eps.data(), &tw, &mid);
+  const size_t tw_bytes = ((tw.size() * sizeof(float2)) + 255) & ~size_t(255);
+  const size_t bytes = tw_bytes + mid.size() * sizeof(float4);
   hipError_t e = hipGetDevice(&p->device);
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->d_tw), sizeof(float2) * n);
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&p->d_mid), sizeof(float2) * n);
-  if (e == hipSuccess) e = hipMemcpy(p->d_tw, tw.data(), sizeof(float2) * n, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemcpy(p->d_mid, mid.data(), sizeof(float2) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMalloc(&p->d_tables, bytes);
+  if (e == hipSuccess) {
+    p->d_tw = static_cast<float2*>(p->d_tables);
+    p->d_mid = reinterpret_cast<float4*>(static_cast<char*>(p->d_tables) + tw_bytes);
+    if (!tw.empty()) e = hipMemcpy(p->d_tw, tw.data(), tw.size() * sizeof(float2), hipMemcpyHostToDevice);
+  }
+  if (e == hipSuccess) e = hipMemcpy(p->d_mid, mid.data(), mid.size() * sizeof(float4), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
-    if (p->d_tw) (void)hipFree(p->d_tw);
-    if (p->d_mid) (void)hipFree(p->d_mid);
+    if (p->d_tables) (void)hipFree(p->d_tables);
     delete p;
     return hip_fail(e, "plan device tables");
   }
@@ -162,8 +209,7 @@ int kashin_plan_destroy(kashin_plan_t plan) {
     std::lock_guard<std::mutex> lk(g_plans_mu);
     if (plan == nullptr || g_plans.erase(plan) == 0) return fail(KASHIN_E_INVALID, "plan is null or destroyed");
   }
-  if (plan->d_tw) (void)hipFree(plan->d_tw);
-  if (plan->d_mid) (void)hipFree(plan->d_mid);
+  if (plan->d_tables) (void)hipFree(plan->d_tables);
   delete plan;
   return ok();
 }

@@ -3,21 +3,22 @@
 
 namespace kashin {
 
-// Supported vector lengths: N, threads per workgroup, forward radices.
+// Supported vector lengths: N, threads per workgroup, occupancy target (waves per SIMD),
+// forward radices.
 #define KASHIN_SIZES(X)          \
-  X(64, 64, 8, 8)                \
-  X(96, 64, 16, 3, 2)            \
-  X(172, 64, 4, 43)              \
-  X(256, 64, 16, 16)             \
-  X(512, 64, 8, 8, 8)            \
-  X(768, 64, 16, 16, 3)          \
-  X(1024, 64, 16, 16, 4)         \
-  X(2048, 128, 16, 16, 8)        \
-  X(3072, 192, 16, 16, 4, 3)     \
-  X(4096, 256, 16, 16, 16)       \
-  X(8192, 512, 16, 16, 16, 2)    \
-  X(11008, 704, 16, 16, 43)      \
-  X(16384, 1024, 16, 16, 16, 4)
+  X(64, 64, 2, 8, 8)                \
+  X(96, 64, 2, 16, 3, 2)            \
+  X(172, 64, 2, 4, 43)              \
+  X(256, 64, 2, 16, 16)             \
+  X(512, 64, 4, 8, 8, 8)            \
+  X(768, 64, 3, 16, 16, 3)          \
+  X(1024, 64, 2, 16, 16, 4)         \
+  X(2048, 128, 2, 16, 16, 8)        \
+  X(3072, 192, 3, 16, 16, 4, 3)     \
+  X(4096, 256, 3, 16, 16, 16)       \
+  X(8192, 512, 2, 16, 16, 16, 2)    \
+  X(11008, 704, 3, 16, 16, 43)      \
+  X(16384, 1024, 4, 16, 16, 16, 4)
 
 #define X(N, ...) hipError_t launch_n##N(const KArgs& a, int64_t grid, hipStream_t stream);
 KASHIN_SIZES(X)
@@ -97,6 +98,24 @@ __global__ __launch_bounds__(CT) void cluster_kernel(ClusterArgs a, int64_t row0
 
 }  // namespace
 
+bool plan_shape(int n, PlanShape* out) {
+  switch (n) {
+#define X(N, T, W, ...)                               \
+  case N: {                                           \
+    const int r[] = {__VA_ARGS__};                    \
+    out->n = N;                                       \
+    out->threads = T;                                 \
+    out->np = static_cast<int>(sizeof(r) / sizeof(int)); \
+    for (int i = 0; i < out->np; ++i) out->rad[i] = r[i]; \
+    return true;                                      \
+  }
+    KASHIN_SIZES(X)
+#undef X
+    default:
+      return false;
+  }
+}
+
 bool supported_n(int n) {
   switch (n) {
 #define X(N, ...) \
@@ -111,8 +130,8 @@ bool supported_n(int n) {
 
 hipError_t launch_pair(int n, const KArgs& a, int64_t grid, hipStream_t stream) {
   switch (n) {
-#define X(N, T, ...) \
-  case N:            \
+#define X(N, ...) \
+  case N:         \
     return launch_n##N(a, grid, stream);
     KASHIN_SIZES(X)
 #undef X

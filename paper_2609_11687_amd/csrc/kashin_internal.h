@@ -18,8 +18,8 @@ enum Mode : int32_t {
 // Everything a launch needs, passed to the kernel by value.
 struct KArgs {
   // operator tables (plan-owned, device)
-  const float2* tw;    // tw[e] = exp(-2 pi i e / N), e in [0, N)
-  const float2* mid;   // eps-folded frequency factors f_k; f_k.y != 0 marks a read from N - k
+  const float2* tw;    // per-pass twiddle tables (layout: see build_tables in kashin_api.cpp)
+  const float4* mid4;  // first inverse pass, per (j, r): {f.x, f.y, LDS byte address of the source, 0}
   int32_t iters;       // blocks of Alg. 2
   int32_t mode;
   int32_t dtype;       // input dtype (KASHIN_F32 / KASHIN_F16)
@@ -58,6 +58,16 @@ struct ClusterArgs {
   uint8_t* codes_v;
   float* centers;
 };
+
+// Radix plan of the pair kernel for vector length n: threads per workgroup and the radices
+// of the forward FFT passes.
+struct PlanShape {
+  int n = 0;
+  int threads = 0;
+  int np = 0;
+  int rad[8] = {};
+};
+bool plan_shape(int n, PlanShape* out);
 
 bool supported_n(int n);
 // Launch the pair kernel for vector length n; grid = number of work items (pairs or listed rows).

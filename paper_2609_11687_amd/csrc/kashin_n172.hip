@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(172, 64, 4, 43)
+KASHIN_DEFINE_SIZE(172, 64, 2, 4, 43)
 }  // namespace kashin

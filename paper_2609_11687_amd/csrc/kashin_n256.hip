@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(256, 64, 16, 16)
+KASHIN_DEFINE_SIZE(256, 64, 2, 16, 16)
 }  // namespace kashin

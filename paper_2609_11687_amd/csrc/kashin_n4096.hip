@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(4096, 256, 16, 16, 16)
+KASHIN_DEFINE_SIZE(4096, 256, 3, 16, 16, 16)
 }  // namespace kashin

@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(64, 64, 8, 8)
+KASHIN_DEFINE_SIZE(64, 64, 2, 8, 8)
 }  // namespace kashin

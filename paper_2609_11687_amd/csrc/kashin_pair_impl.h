@@ -111,22 +111,24 @@ __device__ __forceinline__ void dft_pow2(float2 (&a)[R]) {
 }
 
 // In-register DFT of an odd length R, directly from its definition, pairing j with R-j
-// so each constant multiplies a sum or a difference.
-// Outputs are handed to sink(q, A_q) as soon as they are formed, so they never occupy
-// registers next to the inputs.
-template <int R, bool INV, class Sink>
-__device__ __forceinline__ void dft_odd(const float2 (&a)[R], Sink&& sink) {
+// so each constant multiplies a sum or a difference.  The sums and differences overwrite
+// the inputs in place (a[j] <- a[j] + a[R-j], a[R-j] <- a[j] - a[R-j]) and outputs are
+// handed to sink(q, A_q) as soon as they are formed, so no second array is live.
+// `pre(r, v)` is applied to input r just before it is paired (the pass twiddles), so a
+// twiddled input never waits in a register of its own.
+template <int R, bool INV, class Pre, class Sink>
+__device__ __forceinline__ void dft_odd(float2 (&a)[R], Pre&& pre, Sink&& sink) {
   constexpr int H = (R - 1) / 2;
-  float2 s[H], d[H];
   sfor<1, H + 1>([&](auto jv) {
     constexpr int j = decltype(jv)::value;
-    s[j - 1] = cadd(a[j], a[R - j]);
-    d[j - 1] = csub(a[j], a[R - j]);
+    const float2 p = pre(j, a[j]), m = pre(R - j, a[R - j]);
+    a[j] = cadd(p, m);
+    a[R - j] = csub(p, m);
+    if constexpr (R > 16 && j % 4 == 0) __builtin_amdgcn_sched_barrier(0);
   });
   const float2 x0 = a[0];
   float2 sum = x0;
-  sfor<0, H>([&](auto jv) { sum = cadd(sum, s[decltype(jv)::value]); });
-  sink(0, sum);
+  sfor<1, H + 1>([&](auto jv) { sum = cadd(sum, a[decltype(jv)::value]); });
   sfor<1, H + 1>([&](auto qv) {
     constexpr int q = decltype(qv)::value;
     float2 re = x0;
@@ -136,17 +138,21 @@ __device__ __forceinline__ void dft_odd(const float2 (&a)[R], Sink&& sink) {
       constexpr int m = (j * q) % R;
       constexpr float c = OddTab<R>::c[m];
       constexpr float sn = OddTab<R>::s[m];
-      re.x = fmaf(s[j - 1].x, c, re.x);
-      re.y = fmaf(s[j - 1].y, c, re.y);
-      im.x = fmaf(d[j - 1].x, sn, im.x);
-      im.y = fmaf(d[j - 1].y, sn, im.y);
+      re.x = fmaf(a[j].x, c, re.x);
+      re.y = fmaf(a[j].y, c, re.y);
+      im.x = fmaf(a[R - j].x, sn, im.x);
+      im.y = fmaf(a[R - j].y, sn, im.y);
     });
     // forward: A_q = re - i im, A_{R-q} = re + i im; inverse swaps them
     const float2 minus = make_float2(re.x + im.y, re.y - im.x);
     const float2 plus = make_float2(re.x - im.y, re.y + im.x);
     sink(q, INV ? plus : minus);
     sink(R - q, INV ? minus : plus);
+    // keep the scheduler from interleaving all output pairs (each pair needs its own
+    // accumulators next to the R inputs)
+    if constexpr (R > 16) __builtin_amdgcn_sched_barrier(0);
   });
+  sink(0, sum);
 }
 
 // DFT of a[] handed to sink(q, A_q) for every q (power-of-two R: computed in place first).
@@ -157,19 +163,21 @@ __device__ __forceinline__ void dft(float2 (&a)[R], Sink&& sink) {
     sfor<0, R>([&](auto qv) { sink(decltype(qv)::value, a[decltype(qv)::value]); });
   } else {
     static_assert(R % 2 == 1, "composite non-power-of-two radices are not implemented");
-    dft_odd<R, INV>(a, sink);
+    dft_odd<R, INV>(a, [](int, float2 v) { return v; }, sink);
   }
 }
 
 // ------------------------------------------------------------------ launch configuration
 // N: vector length = complex FFT length of a packed pair.  T: threads per workgroup.
+// W: occupancy target (waves per SIMD) given to the register allocator.
 // Rs: radices of the forward FFT passes; the first radix also fixes the register layout
 // in which the greedy steps run: thread t holds elements j + r * (N / R0) for its
 // butterflies j = t + T * i, r < R0.
-template <int N_, int T_, int... Rs>
+template <int N_, int T_, int W_, int... Rs>
 struct Cfg {
   static constexpr int N = N_;
   static constexpr int T = T_;
+  static constexpr int W = W_;  // waves per SIMD the register allocation must allow
   static constexpr int NP = sizeof...(Rs);
   static constexpr int rad[NP] = {Rs...};
   static constexpr int R0 = rad[0];
@@ -193,19 +201,16 @@ constexpr int ns_inv(int p) {
   return s;
 }
 
-__device__ __forceinline__ int pad(int i) { return i + (i >> 4); }  // one spare slot per 16
+// LDS layout: element k of the length-N complex vector lives at float2 slot pad(k) (one
+// spare slot per 16 elements, so stride-16 accesses of a Stockham pass spread over banks).
+__host__ __device__ constexpr int pad(int i) { return i + (i >> 4); }
 
-// Opaque copies: values (thread index, table pointers) that would otherwise be proven
-// invariant across the block loop and hoisted out of it, keeping every twiddle and
-// address of every pass live in registers at once.
+// Opaque copy of the thread index: without it every twiddle load and LDS address of every
+// pass is proven invariant across the block loop, hoisted out of it, and kept live in
+// registers at once.
 __device__ __forceinline__ int opaque(int v) {
   asm volatile("" : "+v"(v));
   return v;
-}
-template <class P>
-__device__ __forceinline__ P* opaque_ptr(P* p) {
-  asm volatile("" : "+s"(p));
-  return p;
 }
 
 // Position m of the even/odd order -> index in the row.
@@ -215,20 +220,40 @@ __device__ __forceinline__ int orig_index(int m) {
 }
 
 // ------------------------------------------------------------------ reductions
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+// Cross-lane moves with DPP (no LDS round trip).  update_dpp(old = 0, ...): lanes of rows
+// outside ROW_MASK keep 0.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf, false));
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+__device__ __forceinline__ float lane63(float v) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
-// Sum of K values over the workgroup, in a fixed order (every thread gets the same bits).
-// `red` holds 2 * NW * KMAX floats; consecutive calls alternate halves so that one
-// barrier per call suffices.
+// Sum over the wave in a fixed order: quad xor 1, 2, half-row mirror, row mirror, then the
+// row sums folded into lane 63 by row broadcasts; returned as a wave-uniform value.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp<0xb1>(v);       // quad_perm [1,0,3,2]
+  v += dpp<0x4e>(v);       // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);      // row_half_mirror
+  v += dpp<0x140>(v);      // row_mirror
+  v += dpp<0x142, 0xa>(v); // row_bcast:15 into rows 1 and 3
+  v += dpp<0x143, 0xc>(v); // row_bcast:31 into rows 2 and 3
+  return lane63(v);
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp<0xb1>(v));
+  v = fmaxf(v, dpp<0x4e>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  v = fmaxf(v, dpp<0x142, 0xa>(v));
+  v = fmaxf(v, dpp<0x143, 0xc>(v));
+  return lane63(v);
+}
+
+// Sum of K values over the workgroup in a fixed order (every thread gets the same bits).
+// `red` holds 2 * NW * 32 floats; consecutive calls alternate halves, so one barrier per
+// call suffices.
 template <int T, int K>
 __device__ __forceinline__ void block_sum(float (&v)[K], float* red, int& slot) {
 #pragma unroll
@@ -245,6 +270,7 @@ __device__ __forceinline__ void block_sum(float (&v)[K], float* red, int& slot) 
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       float s = r[k];
+#pragma unroll
       for (int w = 1; w < NW; ++w) s += r[w * K + k];
       v[k] = s;
     }
@@ -267,10 +293,38 @@ __device__ __forceinline__ void block_max(float (&v)[K], float* red, int& slot) 
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       float s = r[k];
+#pragma unroll
       for (int w = 1; w < NW; ++w) s = fmaxf(s, r[w * K + k]);
       v[k] = s;
     }
   }
+}
+
+// ------------------------------------------------------------------ plan tables
+// Twiddle tables, one per pass with stride NS > 1, forward passes first then inverse
+// passes: entry [jm][r] = w_N^(r * jm * N / (NS R)), jm < NS, r < R (each table padded to
+// an even length so every table starts 16-byte aligned).  Every thread reads its R
+// twiddles contiguously.
+template <class C, bool INV>
+constexpr int pass_radix(int p) {
+  return INV ? C::rad[C::NP - 1 - p] : C::rad[p];
+}
+template <class C, bool INV>
+constexpr int pass_ns(int p) {
+  return INV ? ns_inv<C>(p) : ns_fwd<C>(p);
+}
+template <class C, bool INV>
+constexpr int tw_offset(int p) {
+  int off = 0;
+  for (int q = 1; q < C::NP; ++q) {
+    if (!INV && q == p) return off;
+    off += (ns_fwd<C>(q) * C::rad[q] + 1) & ~1;
+  }
+  for (int q = 1; q < C::NP; ++q) {
+    if (INV && q == p) return off;
+    off += (ns_inv<C>(q) * C::rad[C::NP - 1 - q] + 1) & ~1;
+  }
+  return off;
 }
 
 // ------------------------------------------------------------------ FFT passes
@@ -279,41 +333,45 @@ enum { DST_LDS = 0, DST_REGS = 1 };
 
 // One Stockham pass of radix R with stride NS: butterfly j reads elements j + r * N/R,
 // multiplies by the twiddles w_N^(r * (j mod NS) * N/(NS R)), takes a length-R DFT, and
-// writes element q to (j / NS) * NS * R + (j mod NS) + q * NS.  In-place in LDS: every
-// read completes (barrier) before any write.  SRC_MID applies the eps gather-and-scale
-// on the way in (first inverse pass).
-template <class C, int R, int NS, bool INV, int SRC, int DST>
+// writes element q to (j / NS) * NS * R + (j mod NS) + q * NS.  In place in LDS: every
+// read completes (barrier) before any write.  SRC_MID (first inverse pass) reads through
+// the eps table: element k = j + r N/R comes from LDS byte address mid[j R + r].z, scaled by
+// the complex factor mid[j R + r].xy.
+template <class C, int P, bool INV, int SRC, int DST>
 __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__ lds,
-                                         const float2* __restrict__ tw, const float2* __restrict__ mid) {
+                                         const float2* __restrict__ tw, const float4* __restrict__ mid) {
   constexpr int N = C::N;
   constexpr int T = C::T;
+  constexpr int R = pass_radix<C, INV>(P);
+  constexpr int NS = pass_ns<C, INV>(P);
   constexpr int NB = N / R;
   constexpr int BP = (NB + T - 1) / T;
+  constexpr bool FULL = (NB % T) == 0;
   static_assert(SRC != SRC_REGS || (R == C::R0 && NS == 1), "register source must be the first pass");
   static_assert(DST != DST_REGS || (R == C::R0 && NS == N / C::R0), "register target must be the last pass");
   const int tid = opaque(static_cast<int>(threadIdx.x));
-  tw = opaque_ptr(tw);
-  mid = opaque_ptr(mid);
   float2 a[BP][R];
   sfor<0, BP>([&](auto iv) {
     constexpr int i = decltype(iv)::value;
     const int j = tid + T * i;
     if constexpr (SRC == SRC_REGS) {
       sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = z[i * R + decltype(rv)::value]; });
-    } else {
-      if (NB % T == 0 || j < NB) {
+    } else if (FULL || j < NB) {
+      if constexpr (SRC == SRC_MID) {
+        const float4* m = mid + j * R;
+        const char* lb = reinterpret_cast<const char*>(lds);
         sfor<0, R>([&](auto rv) {
           constexpr int r = decltype(rv)::value;
-          const int k = j + r * NB;
-          if constexpr (SRC == SRC_MID) {
-            const float2 f = mid[k];
-            const int src = (f.y != 0.f) ? (N - k) : k;
-            const float2 v = lds[pad(src)];
-            a[i][r] = make_float2(f.x * v.x - f.y * v.y, f.x * v.y + f.y * v.x);
-          } else {
-            a[i][r] = lds[pad(k)];
-          }
+          const float4 f = m[r];
+          const float2 v = *reinterpret_cast<const float2*>(lb + __float_as_int(f.z));
+          a[i][r] = make_float2(f.x * v.x - f.y * v.y, f.x * v.y + f.y * v.x);
+          if constexpr (R > 16 && r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
         });
+      } else if constexpr (NB % 16 == 0) {
+        const float2* base = lds + pad(j);
+        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = base[decltype(rv)::value * pad(NB)]; });
+      } else {
+        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = lds[pad(j + decltype(rv)::value * NB)]; });
       }
     }
   });
@@ -321,20 +379,52 @@ __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__
   sfor<0, BP>([&](auto iv) {
     constexpr int i = decltype(iv)::value;
     const int j = tid + T * i;
-    if (NB % T == 0 || j < NB) {
+    if (FULL || j < NB) {
       const int jm = (NS > 1) ? (j % NS) : 0;
-      if constexpr (NS > 1) {
-        sfor<1, R>([&](auto rv) {
-          constexpr int r = decltype(rv)::value;
-          const float2 w = tw[r * jm * (N / (NS * R))];
-          const float2 v = a[i][r];
-          if constexpr (!INV) a[i][r] = make_float2(v.x * w.x - v.y * w.y, v.x * w.y + v.y * w.x);
-          else a[i][r] = make_float2(v.x * w.x + v.y * w.y, v.y * w.x - v.x * w.y);
-        });
+      if constexpr (NS > 1 && R % 2 == 0) {
+        // a_r *= w_N^(r jm N/(NS R)) (conjugate on the inverse), read pairwise from the
+        // thread's contiguous table row and applied as soon as it arrives
+        const float2* tp = tw + tw_offset<C, INV>(P) + jm * R;
+        auto twmul = [&](float2& v, float2 t) {
+          if constexpr (!INV) v = make_float2(v.x * t.x - v.y * t.y, v.x * t.y + v.y * t.x);
+          else v = make_float2(v.x * t.x + v.y * t.y, v.y * t.x - v.x * t.y);
+        };
+        if constexpr (R % 2 == 0) {
+          const float4* t4 = reinterpret_cast<const float4*>(tp);
+          sfor<0, R / 2>([&](auto hv) {
+            constexpr int h = decltype(hv)::value;
+            const float4 q = t4[h];
+            if constexpr (h > 0) twmul(a[i][2 * h], make_float2(q.x, q.y));
+            twmul(a[i][2 * h + 1], make_float2(q.z, q.w));
+          });
+        }
       }
       if constexpr (DST == DST_LDS) {
-        const int base = (j / NS) * NS * R + jm;
-        dft<R, INV>(a[i], [&](int q, float2 v) { lds[pad(base + q * NS)] = v; });
+        const int idx0 = (j / NS) * NS * R + jm;
+        if constexpr (R % 2 == 1 && NS > 1) {
+          // odd radix: the twiddle of each input is applied inside the DFT's pairing step
+          const float2* tp = tw + tw_offset<C, INV>(P) + jm * R;
+          auto pre = [&](int r, float2 v) {
+            if (r == 0) return v;
+            const float2 t = tp[r];
+            if constexpr (!INV) return make_float2(v.x * t.x - v.y * t.y, v.x * t.y + v.y * t.x);
+            else return make_float2(v.x * t.x + v.y * t.y, v.y * t.x - v.x * t.y);
+          };
+          if constexpr (NS % 16 == 0) {
+            float2* base = lds + pad(idx0);
+            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { base[q * pad(NS)] = v; });
+          } else {
+            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+          }
+        } else if constexpr (NS % 16 == 0) {
+          float2* base = lds + pad(idx0);
+          dft<R, INV>(a[i], [&](int q, float2 v) { base[q * pad(NS)] = v; });
+        } else if constexpr (NS == 1 && 16 % R == 0) {
+          float2* base = lds + pad(idx0);
+          dft<R, INV>(a[i], [&](int q, float2 v) { base[q] = v; });
+        } else {
+          dft<R, INV>(a[i], [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+        }
       } else {
         dft<R, INV>(a[i], [&](int q, float2 v) { z[i * R + q] = v; });
       }
@@ -344,31 +434,209 @@ __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__
 }
 
 template <class C, int P>
-__device__ __forceinline__ void fwd_passes(float2 (&z)[C::E], float2* lds, const float2* tw, const float2* mid) {
+__device__ __forceinline__ void fwd_passes(float2 (&z)[C::E], float2* lds, const float2* tw, const float4* mid) {
   if constexpr (P < C::NP) {
-    fft_pass<C, C::rad[P], ns_fwd<C>(P), false, (P == 0 ? SRC_REGS : SRC_LDS), DST_LDS>(z, lds, tw, mid);
+    fft_pass<C, P, false, (P == 0 ? SRC_REGS : SRC_LDS), DST_LDS>(z, lds, tw, mid);
     fwd_passes<C, P + 1>(z, lds, tw, mid);
   }
 }
 template <class C, int P>
-__device__ __forceinline__ void inv_passes(float2 (&z)[C::E], float2* lds, const float2* tw, const float2* mid) {
+__device__ __forceinline__ void inv_passes(float2 (&z)[C::E], float2* lds, const float2* tw, const float4* mid) {
   if constexpr (P < C::NP) {
-    fft_pass<C, C::rad[C::NP - 1 - P], ns_inv<C>(P), true, (P == 0 ? SRC_MID : SRC_LDS),
-             (P == C::NP - 1 ? DST_REGS : DST_LDS)>(z, lds, tw, mid);
+    fft_pass<C, P, true, (P == 0 ? SRC_MID : SRC_LDS), (P == C::NP - 1 ? DST_REGS : DST_LDS)>(z, lds, tw, mid);
     inv_passes<C, P + 1>(z, lds, tw, mid);
   }
 }
 
 // z <- P z for both rows of the pair (Alg. 2: P z = IDCT(eps * DCT(z))).
 template <class C>
-__device__ __forceinline__ void apply_P(float2 (&z)[C::E], float2* lds, const float2* tw, const float2* mid) {
+__device__ __forceinline__ void apply_P(float2 (&z)[C::E], float2* lds, const float2* tw, const float4* mid) {
   fwd_passes<C, 0>(z, lds, tw, mid);
   inv_passes<C, 0>(z, lds, tw, mid);
 }
 
+// ------------------------------------------------------------------ resident-table path
+// Launch shapes whose passes all use one power-of-two radix R <= 16 with exactly one
+// butterfly per thread (T == N/R, N/R a multiple of 16) keep the operator's constants out
+// of memory inside the block loop: the twiddles of the last pass (stride N/R, one row
+// of R per thread) and the eps factors of the middle step live in registers, loaded once;
+// the smaller twiddle tables of the inner passes are copied to LDS once.  The forward
+// last pass, the eps step and the inverse first pass are fused: thread t holds Y_k for
+// k = t + q N/R after the forward FFT and needs exactly those elements for the inverse
+// one, plus Y_{N-k}, which thread N/R - t holds; one LDS exchange brings the partner's
+// values, and the element to use is chosen by the factor itself (f_k.y == 0 exactly when
+// eps_k == eps_{N-k}).
+template <class C>
+constexpr bool resident_ok() {
+  for (int p = 0; p < C::NP; ++p)
+    if (C::rad[p] != C::R0) return false;
+  return C::NP >= 2 && C::R0 <= 16 && (C::R0 & (C::R0 - 1)) == 0 && C::T == C::N / C::R0 &&
+         (C::N / C::R0) % 16 == 0;
+}
+// LDS slots (float2) of the inner-pass twiddle tables (passes 1 .. NP-2), after the FFT buffer
+template <class C>
+constexpr int small_tw_offset(int p) {
+  int off = 0;
+  for (int q = 1; q < p; ++q) off += ns_fwd<C>(q) * C::R0;
+  return off;
+}
+template <class C>
+constexpr int small_tw_total() {
+  return resident_ok<C>() ? small_tw_offset<C>(C::NP - 1) : 0;
+}
+
+template <class C>
+struct ResRegs {
+  float2 tw[C::R0];         // w_N^(r t), r < R: twiddles of the last pass (index 0 unused)
+  const float4* mid_row;    // this thread's eps factors: entries k = t + r N/R, r < R
+};
+
+template <class C>
+__device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const float2* __restrict__ tw,
+                                              const float4* __restrict__ mid) {
+  constexpr int R = C::R0;
+  const int t = threadIdx.x;
+  const float4* t4 = reinterpret_cast<const float4*>(tw + tw_offset<C, false>(C::NP - 1) + t * R);
+  sfor<0, R / 2>([&](auto hv) {
+    constexpr int h = decltype(hv)::value;
+    const float4 q = t4[h];
+    rr.tw[2 * h] = make_float2(q.x, q.y);
+    rr.tw[2 * h + 1] = make_float2(q.z, q.w);
+  });
+  rr.mid_row = mid + t * R;
+  // inner-pass tables, transposed to [r][jm] so that the lanes of a wave (consecutive jm)
+  // read consecutive LDS words (the [jm][r] rows of the global layout are 8R bytes apart,
+  // which would put every lane of a 16-lane group on the same banks)
+  float2* small = lds + C::LDS;
+  sfor<1, C::NP - 1>([&](auto pv) {
+    constexpr int P = decltype(pv)::value;
+    constexpr int NS = ns_fwd<C>(P);
+    constexpr int OFF = small_tw_offset<C>(P);
+    for (int i = t; i < NS * R; i += C::T) {
+      const int jm = i / R, r = i % R;
+      small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
+    }
+  });
+  __syncthreads();
+}
+
+template <bool INV>
+__device__ __forceinline__ float2 twmul(float2 v, float2 t) {
+  if constexpr (!INV) return make_float2(v.x * t.x - v.y * t.y, v.x * t.y + v.y * t.x);
+  else return make_float2(v.x * t.x + v.y * t.y, v.y * t.x - v.x * t.y);
+}
+
+// Inner pass p (1 <= p <= NP-2) of the resident path: stride NS = R^p, LDS -> LDS,
+// twiddles from the LDS copy of the pass-p table.
+template <class C, int P, bool INV>
+__device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) {
+  constexpr int R = C::R0;
+  constexpr int NB = C::N / R;
+  constexpr int NS = ns_fwd<C>(P);
+  float2 a[R];
+  const float2* rb = lds + pad(t);
+  sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+  __syncthreads();
+  const int jm = t % NS;
+  const float2* tb = lds + C::LDS + small_tw_offset<C>(P) + jm;  // table [r][jm]
+  sfor<1, R>([&](auto rv) {
+    constexpr int r = decltype(rv)::value;
+    a[r] = twmul<INV>(a[r], tb[r * NS]);
+  });
+  const int idx0 = (t / NS) * NS * R + jm;
+  float2* wb = lds + pad(idx0);
+  static_assert(NS % 16 == 0 || (NS * R) % 16 == 0, "inner pass stride");
+  if constexpr (NS % 16 == 0) {
+    dft<R, INV>(a, [&](int q, float2 v) { wb[q * pad(NS)] = v; });
+  } else {
+    dft<R, INV>(a, [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+  }
+  __syncthreads();
+}
+
+template <class C, int P, bool INV>
+__device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
+  if constexpr (P >= 1 && P <= C::NP - 2) {
+    // the inverse FFT meets the strides in the same order (R, R^2, ...) as the forward one
+    res_inner_pass<C, P, INV>(lds, t);
+    res_inner_passes<C, P + 1, INV>(lds, t);
+  }
+}
+
+// z <- P z on the resident path.
+template <class C>
+__device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, const ResRegs<C>& rr) {
+  constexpr int N = C::N;
+  constexpr int R = C::R0;
+  constexpr int NB = N / R;
+  constexpr int NP = C::NP;
+  const int t = opaque(static_cast<int>(threadIdx.x));
+  // forward pass 0 (stride 1): registers -> LDS, element q to t R + q
+  {
+    float2 a[R];
+    sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = z[decltype(rv)::value]; });
+    float2* wb = lds + pad(t * R);
+    dft<R, false>(a, [&](int q, float2 v) { wb[q] = v; });
+    __syncthreads();
+  }
+  res_inner_passes<C, 1, false>(lds, t);
+  // forward last pass (stride N/R), fused with the eps step and the inverse first pass
+  float2 y[R];
+  {
+    // eps factors for the fused step, fetched now so their latency overlaps this pass
+    float2 f[R];
+    sfor<0, R>([&](auto rv) {
+      const float4 m = rr.mid_row[decltype(rv)::value];
+      f[decltype(rv)::value] = make_float2(m.x, m.y);
+    });
+    const float2* rb = lds + pad(t);
+    sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+    __syncthreads();
+    sfor<1, R>([&](auto rv) { y[decltype(rv)::value] = twmul<false>(y[decltype(rv)::value], rr.tw[decltype(rv)::value]); });
+    dft_pow2<R, false>(y);  // y[q] = Y_{t + q NB}
+    float2* wb = lds + pad(t);
+    sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NB)] = y[decltype(qv)::value]; });
+    __syncthreads();
+    // partner values Y_{N - t - q NB} (slot pad(N - t) - q pad(NB); for t = 0, q = 0 the
+    // slot just past the buffer is read but never used: k = 0 pairs with itself)
+    const float2* pb = lds + pad(N - t);
+    sfor<0, R>([&](auto qv) {
+      constexpr int q = decltype(qv)::value;
+      const float2 fq = f[q];
+      const float2 own = y[q];
+      const float2 oth = pb[-q * pad(NB)];
+      const float2 v = (fq.y != 0.f) ? oth : own;
+      y[q] = make_float2(fq.x * v.x - fq.y * v.y, fq.x * v.y + fq.y * v.x);
+      if constexpr (q % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
+    });
+    __syncthreads();
+  }
+  // inverse pass 0 (stride 1): element q to t R + q
+  {
+    float2* wb = lds + pad(t * R);
+    dft<R, true>(y, [&](int q, float2 v) { wb[q] = v; });
+    __syncthreads();
+  }
+  res_inner_passes<C, 1, true>(lds, t);
+  // inverse last pass (stride N/R): LDS -> registers
+  {
+    const float2* rb = lds + pad(t);
+    sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+    sfor<1, R>([&](auto rv) { z[decltype(rv)::value] = twmul<true>(z[decltype(rv)::value], rr.tw[decltype(rv)::value]); });
+    dft_pow2<R, true>(z);
+  }
+}
+
 // ------------------------------------------------------------------ greedy step
-__device__ __forceinline__ float sgn_times(float x, float c) { return x > 0.f ? c : (x < 0.f ? -c : 0.f); }
 __device__ __forceinline__ int8_t sgn8(float x) { return x > 0.f ? 1 : (x < 0.f ? -1 : 0); }
+// sign(x) * c with sign(0) = 0
+__device__ __forceinline__ float sgn_times(float x, float c) { return x == 0.f ? 0.f : copysignf(c, x); }
+
+template <int N>
+__device__ __forceinline__ float div_n(float s) {
+  if constexpr ((N & (N - 1)) == 0) return s * (1.0f / N);  // exact: same bits as s / N
+  else return s / static_cast<float>(N);
+}
 
 // One atomic greedy step of Alg. 2 on both rows: c = ||x||_1 / N, delta = sign(x) c
 // (sign(0) = 0), x -= delta, and acc += delta when ACC.  Returns (c_a, c_b).  With
@@ -383,8 +651,8 @@ __device__ __forceinline__ float2 greedy_step(float2 (&z)[C::E], float2 (&acc)[C
     s[1] += fabsf(z[e].y);
   }
   block_sum<C::T, 2>(s, red, slot);
-  const float ca = s[0] / static_cast<float>(C::N);
-  const float cb = s[1] / static_cast<float>(C::N);
+  const float ca = div_n<C::N>(s[0]);
+  const float cb = div_n<C::N>(s[1]);
   if (trace != nullptr) {
     const int tid = opaque(static_cast<int>(threadIdx.x));
 #pragma unroll
@@ -414,47 +682,52 @@ __device__ __forceinline__ float2 greedy_step(float2 (&z)[C::E], float2 (&acc)[C
 }
 
 // ------------------------------------------------------------------ loads / stores
-__device__ __forceinline__ float ld_elem(const void* p, int64_t idx, int dtype) {
-  if (dtype == 1) return __half2float(static_cast<const __half*>(p)[idx]);
-  return static_cast<const float*>(p)[idx];
-}
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(__half v) { return __half2float(v); }
 
 // Load rows a (and b if >= 0) into the greedy register layout, in even/odd order.
-template <class C>
-__device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
-                                          int64_t rb) {
+template <class C, class IT>
+__device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restrict__ w, int64_t ldw, int64_t ra,
+                                            int64_t rb) {
+  const IT* __restrict__ pa = w + ra * ldw;
+  const IT* __restrict__ pb = w + (rb >= 0 ? rb : ra) * ldw;
 #pragma unroll
   for (int i = 0; i < C::B0; ++i) {
     const int j = threadIdx.x + C::T * i;
 #pragma unroll
     for (int r = 0; r < C::R0; ++r) {
       float2 v = make_float2(0.f, 0.f);
-      if (j < C::NB0) {
+      if (C::NB0 % C::T == 0 || j < C::NB0) {
         const int src = orig_index<C::N>(j + r * C::NB0);
-        v.x = ld_elem(w, ra * ldw + src, dtype);
-        if (rb >= 0) v.y = ld_elem(w, rb * ldw + src, dtype);
+        v.x = to_f32(pa[src]);
+        v.y = to_f32(pb[src]);
       }
       z[i * C::R0 + r] = v;
     }
   }
+  if (rb < 0) {
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) z[e].y = 0.f;
+  }
+}
+
+template <class C>
+__device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
+                                          int64_t rb) {
+  if (dtype == 1) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb);
+  else load_pair_t<C>(z, static_cast<const float*>(w), ldw, ra, rb);
 }
 
 // z <- w * scale - z for the pair (rows reloaded in the register layout); zero for a bad row.
 template <class C>
 __device__ __forceinline__ void sub_from_rows(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
                                               int64_t rb, float2 scale, bool bad_a, bool bad_b) {
+  float2 t[C::E];
+  load_pair<C>(t, w, dtype, ldw, ra, rb);
 #pragma unroll
-  for (int i = 0; i < C::B0; ++i) {
-    const int j = threadIdx.x + C::T * i;
-    if (j < C::NB0) {
-#pragma unroll
-      for (int r = 0; r < C::R0; ++r) {
-        const int src = orig_index<C::N>(j + r * C::NB0);
-        float2& v = z[i * C::R0 + r];
-        v.x = bad_a ? 0.f : fmaf(ld_elem(w, ra * ldw + src, dtype), scale.x, -v.x);
-        v.y = (bad_b || rb < 0) ? 0.f : fmaf(ld_elem(w, rb * ldw + src, dtype), scale.y, -v.y);
-      }
-    }
+  for (int e = 0; e < C::E; ++e) {
+    z[e].x = bad_a ? 0.f : fmaf(t[e].x, scale.x, -z[e].x);
+    z[e].y = bad_b ? 0.f : fmaf(t[e].y, scale.y, -z[e].y);
   }
 }
 
@@ -530,156 +803,19 @@ __device__ __forceinline__ void midpoints(const float (&q)[4], float (&m)[3]) {
   m[2] = (q[2] + q[3]) * 0.5f;
 }
 
-// ------------------------------------------------------------------ greedy kernel
-// Alg. 2 for a pair of rows.  Only the residual z and the accumulated vhat live in
-// registers across the blocks; after the last block (whose final P is skipped) the
-// first factor is recovered exactly as u = w - P(z + vhat), since w = u + P vhat + P z.
-// LLOYD selects the instance with k-means refinement after the closed form; the
-// closed-form-only instance (a.lloyd == 0) carries none of its registers.
+// Closed-form centres of both rows from the two step sizes of block 0 (Sec. 3.1), then
+// `lloyd` plain 1-D k-means passes when LLOYD (an emptied cluster keeps its centre;
+// centres re-sorted after each pass).  q[side][4], ascending.
 template <class C, bool LLOYD>
-__global__ __launch_bounds__(C::T) void pair_greedy_kernel(KArgs a, int64_t item0) {
-  __shared__ float2 lds[C::LDS];
-  __shared__ float red[2 * C::NW * 32];
-  const int64_t item = item0 + blockIdx.x;
-  int64_t ra;
-  int side = 0;
-  if (a.mode == MODE_TRACE) {
-    const int64_t row = a.rows[item];
-    if (row < 0 || row >= a.m) return;  // uniform: the whole workgroup reads the same entry
-    ra = row & ~int64_t(1);
-    side = static_cast<int>(row & 1);
-  } else {
-    ra = 2 * item;
-  }
-  const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
-  int slot = 0;
-
-  float2 z[C::E], vh[C::E];
-  load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
-  float2 scale, unscale;
-  bool bad_a, bad_b;
-  normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
-#pragma unroll
-  for (int e = 0; e < C::E; ++e) vh[e] = make_float2(0.f, 0.f);
-
-  const int steps = 4 * a.iters;
-  int8_t* trace = nullptr;
-  float* trc = nullptr;
-  if (a.mode == MODE_TRACE) {
-    trace = a.tr_signs + (item * steps) * int64_t(C::N);
-    trc = a.tr_c + item * steps;
-  }
-  float2 cs[4];
-  float2 csum_u = make_float2(0.f, 0.f), csum_v = make_float2(0.f, 0.f);
-  for (int t = 0; t < a.iters; ++t) {
-    if (t > 0) apply_P<C>(z, lds, a.tw, a.mid);  // back to the residual rho
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      if (st == 2) apply_P<C>(z, lds, a.tw, a.mid);  // z = P rho
-      int8_t* tr = trace ? trace + int64_t(4 * t + st) * C::N : nullptr;
-      const float2 c = (st < 2) ? greedy_step<C, false>(z, vh, red, slot, tr, side)
-                                : greedy_step<C, true>(z, vh, red, slot, tr, side);
-      if (t == 0) cs[st] = c;
-      if (st < 2) csum_u = cadd(csum_u, c);
-      else csum_v = cadd(csum_v, c);
-      if (trc != nullptr && threadIdx.x == 0) trc[4 * t + st] = (side ? c.y : c.x) * (side ? unscale.y : unscale.x);
-    }
-  }
-
-  // u = w - P(z + vhat): z <- P(z + vhat), then u = w_scaled - z (row reloaded from HBM).
-  const bool want_r = (a.mode == MODE_DECOMPOSE) && a.r != nullptr;
-#pragma unroll
-  for (int e = 0; e < C::E; ++e) z[e] = cadd(z[e], vh[e]);
-  apply_P<C>(z, lds, a.tw, a.mid);
-  sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
-  // now z holds u (scaled)
-  float2 (&u)[C::E] = z;
-
-  const float qnan = __int_as_float(0x7fc00000);
-  if (a.mode == MODE_DECOMPOSE || a.mode == MODE_TRACE) {
-    bool wa = true, wb = rb >= 0;
-    int64_t oa = ra, ob = rb;
-    if (a.mode == MODE_TRACE) {
-      wa = side == 0;
-      wb = side == 1;
-      oa = ob = item;
-    }
-    for_each_elem<C>([&](int e, int i) {
-      if (wa) {
-        a.u[oa * C::N + i] = bad_a ? qnan : u[e].x * unscale.x;
-        a.vhat[oa * C::N + i] = bad_a ? qnan : vh[e].x * unscale.x;
-      }
-      if (wb) {
-        a.u[ob * C::N + i] = bad_b ? qnan : u[e].y * unscale.y;
-        a.vhat[ob * C::N + i] = bad_b ? qnan : vh[e].y * unscale.y;
-      }
-    });
-    if (a.mode == MODE_DECOMPOSE && a.bounds != nullptr) {
-      float mx[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int e = 0; e < C::E; ++e) {
-        mx[0] = fmaxf(mx[0], fabsf(u[e].x));
-        mx[1] = fmaxf(mx[1], fabsf(vh[e].x));
-        mx[2] = fmaxf(mx[2], fabsf(u[e].y));
-        mx[3] = fmaxf(mx[3], fabsf(vh[e].y));
-      }
-      block_max<C::T, 4>(mx, red, slot);
-      if (threadIdx.x == 0) {
-        float* b = a.bounds + ra * 4;
-        b[0] = bad_a ? qnan : mx[0] * unscale.x;
-        b[1] = bad_a ? qnan : mx[1] * unscale.x;
-        b[2] = bad_a ? qnan : csum_u.x * unscale.x;
-        b[3] = bad_a ? qnan : csum_v.x * unscale.x;
-        if (rb >= 0) {
-          b[4] = bad_b ? qnan : mx[2] * unscale.y;
-          b[5] = bad_b ? qnan : mx[3] * unscale.y;
-          b[6] = bad_b ? qnan : csum_u.y * unscale.y;
-          b[7] = bad_b ? qnan : csum_v.y * unscale.y;
-        }
-      }
-    }
-    if (a.mode == MODE_DECOMPOSE && a.cstep != nullptr && threadIdx.x == 0) {
-      float* c = a.cstep + ra * 4;
-#pragma unroll
-      for (int st = 0; st < 4; ++st) c[st] = bad_a ? qnan : cs[st].x * unscale.x;
-      if (rb >= 0) {
-#pragma unroll
-        for (int st = 0; st < 4; ++st) c[4 + st] = bad_b ? qnan : cs[st].y * unscale.y;
-      }
-    }
-    if (want_r) {
-      // r = P z_final = w - u - P vhat: z <- P vhat (vhat moved in first), then r = w - u - z.
-#pragma unroll
-      for (int e = 0; e < C::E; ++e) {
-        const float2 t = vh[e];
-        vh[e] = u[e];  // keep u
-        u[e] = t;
-      }
-      apply_P<C>(z, lds, a.tw, a.mid);  // z = P vhat
-      sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);  // z = w - P vhat
-      for_each_elem<C>([&](int e, int i) {
-        a.r[ra * C::N + i] = bad_a ? qnan : (z[e].x - vh[e].x) * unscale.x;
-        if (rb >= 0) a.r[rb * C::N + i] = bad_b ? qnan : (z[e].y - vh[e].y) * unscale.y;
-      });
-    }
-    return;
-  }
-
-  // MODE_QUANTIZE: four-peak clustering of u and vhat for both rows (Sec. 3.1), in the
-  // scaled domain (a power-of-two scale changes no comparison and no mean).
-  // q[f][s]: factor f (0 = u, 1 = vhat), side s (0 = row a, 1 = row b).
-  float q[2][2][4];
-  closed_form(cs[0].x, cs[1].x, q[0][0]);
-  closed_form(cs[0].y, cs[1].y, q[0][1]);
-  closed_form(cs[2].x, cs[3].x, q[1][0]);
-  closed_form(cs[2].y, cs[3].y, q[1][1]);
-  for (int it = 0; LLOYD && it < a.lloyd; ++it) {
-#pragma unroll
-    for (int f = 0; f < 2; ++f) {
-      float2(&x)[C::E] = f ? vh : u;
+__device__ __forceinline__ void cluster_factor(const float2 (&x)[C::E], float2 c1, float2 c2, int lloyd, float* red,
+                                               int& slot, float (&q)[2][4]) {
+  closed_form(c1.x, c2.x, q[0]);
+  closed_form(c1.y, c2.y, q[1]);
+  if constexpr (LLOYD) {
+    for (int it = 0; it < lloyd; ++it) {
       float mids[2][3];
-      midpoints(q[f][0], mids[0]);
-      midpoints(q[f][1], mids[1]);
+      midpoints(q[0], mids[0]);
+      midpoints(q[1], mids[1]);
       float acc[16];
 #pragma unroll
       for (int k = 0; k < 16; ++k) acc[k] = 0.f;
@@ -700,56 +836,236 @@ __global__ __launch_bounds__(C::T) void pair_greedy_kernel(KArgs a, int64_t item
       for (int sd = 0; sd < 2; ++sd) {
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-          if (acc[sd * 8 + 4 + c] > 0.f) q[f][sd][c] = acc[sd * 8 + c] / acc[sd * 8 + 4 + c];
-        sort4(q[f][sd]);
+          if (acc[sd * 8 + 4 + c] > 0.f) q[sd][c] = acc[sd * 8 + c] / acc[sd * 8 + 4 + c];
+        sort4(q[sd]);
       }
     }
   }
-  float mids[2][2][3];
-#pragma unroll
-  for (int f = 0; f < 2; ++f)
-#pragma unroll
-    for (int s = 0; s < 2; ++s) midpoints(q[f][s], mids[f][s]);
-  // codes in row order into LDS (four byte planes: [f][s][N]), then pack four per byte.
+}
+
+// 2-bit codes of both rows (code = number of midpoints strictly below the value), staged
+// in LDS in row order and packed four per byte: byte b holds elements 4b..4b+3, element
+// 4b+k in bits 2k.  Leaves the LDS free (barrier on exit).
+template <class C>
+__device__ __forceinline__ void write_codes(const float2 (&x)[C::E], const float (&q)[2][4], float2* lds,
+                                            uint8_t* dst, int64_t ra, int64_t rb, bool bad_a, bool bad_b) {
+  float mids[2][3];
+  midpoints(q[0], mids[0]);
+  midpoints(q[1], mids[1]);
   uint8_t* cb = reinterpret_cast<uint8_t*>(lds);
+  __syncthreads();  // the last FFT pass read this buffer without a closing barrier
   for_each_elem<C>([&](int e, int i) {
-    cb[0 * C::N + i] = static_cast<uint8_t>(code_of(u[e].x, mids[0][0]));
-    cb[1 * C::N + i] = static_cast<uint8_t>(code_of(u[e].y, mids[0][1]));
-    cb[2 * C::N + i] = static_cast<uint8_t>(code_of(vh[e].x, mids[1][0]));
-    cb[3 * C::N + i] = static_cast<uint8_t>(code_of(vh[e].y, mids[1][1]));
+    cb[i] = static_cast<uint8_t>(code_of(x[e].x, mids[0]));
+    cb[C::N + i] = static_cast<uint8_t>(code_of(x[e].y, mids[1]));
   });
   __syncthreads();
   constexpr int NBY = (C::N + 3) / 4;
   for (int b = threadIdx.x; b < NBY; b += C::T) {
 #pragma unroll
-    for (int plane = 0; plane < 4; ++plane) {
-      const int s = plane & 1;
-      const int64_t row = s ? rb : ra;
+    for (int sd = 0; sd < 2; ++sd) {
+      const int64_t row = sd ? rb : ra;
       if (row < 0) continue;
-      const bool bad = s ? bad_b : bad_a;
-      uint8_t byte = 0;
+      uint32_t byte = 0;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int i = 4 * b + k;
-        if (i < C::N) byte |= static_cast<uint8_t>((cb[plane * C::N + i] & 3) << (2 * k));
+        if (C::N % 4 == 0 || i < C::N) byte |= static_cast<uint32_t>(cb[sd * C::N + i] & 3) << (2 * k);
       }
-      uint8_t* dst = (plane < 2) ? a.codes_u : a.codes_v;
-      dst[row * NBY + b] = bad ? 0 : byte;
+      dst[row * NBY + b] = (sd ? bad_b : bad_a) ? 0 : static_cast<uint8_t>(byte);
     }
   }
-  if (threadIdx.x == 0) {
+  __syncthreads();
+}
+
+__device__ __forceinline__ void store_centers(float* centers, int f, const float (&q)[2][4], int64_t ra, int64_t rb,
+                                              float2 unscale, bool bad_a, bool bad_b) {
+  const float qnan = __int_as_float(0x7fc00000);
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int64_t row = s ? rb : ra;
-      if (row < 0) continue;
-      const bool bad = s ? bad_b : bad_a;
-      const float us = s ? unscale.y : unscale.x;
-      float* ce = a.centers + row * 8;
+  for (int c = 0; c < 4; ++c) centers[ra * 8 + f * 4 + c] = bad_a ? qnan : q[0][c] * unscale.x;
+  if (rb >= 0) {
 #pragma unroll
-      for (int f = 0; f < 2; ++f)
+    for (int c = 0; c < 4; ++c) centers[rb * 8 + f * 4 + c] = bad_b ? qnan : q[1][c] * unscale.y;
+  }
+}
+
+// ------------------------------------------------------------------ greedy kernel
+// Alg. 2 for a pair of rows.  Only the residual z and the accumulated vhat live in
+// registers across the blocks; after the last block (whose final P is skipped) the
+// first factor is recovered exactly as u = w - P(z + vhat), since w = u + P vhat + P z.
+// LLOYD selects the instance with k-means refinement after the closed form; the
+// closed-form-only instance (a.lloyd == 0) carries none of its registers.
+template <class C, bool LLOYD>
+__global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_greedy_kernel(
+    KArgs a, int64_t item0) {
+  __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
+  __shared__ float red[2 * C::NW * 32];
+  const int64_t item = item0 + blockIdx.x;
+  int64_t ra;
+  int side = 0;
+  if (a.mode == MODE_TRACE) {
+    const int64_t row = a.rows[item];
+    if (row < 0 || row >= a.m) return;  // uniform: the whole workgroup reads the same entry
+    ra = row & ~int64_t(1);
+    side = static_cast<int>(row & 1);
+  } else {
+    ra = 2 * item;
+  }
+  const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
+  int slot = 0;
+
+  constexpr bool RES = resident_ok<C>();
+  ResRegs<C> rr;
+  if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
+  auto applyP = [&](float2(&v)[C::E]) {
+    if constexpr (RES) apply_P_res<C>(v, lds, rr);
+    else apply_P<C>(v, lds, a.tw, a.mid4);
+  };
+
+  float2 z[C::E], vh[C::E];
+  load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
+  float2 scale, unscale;
+  bool bad_a, bad_b;
+  normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) ce[f * 4 + c] = bad ? qnan : q[f][s][c] * us;
+  for (int e = 0; e < C::E; ++e) vh[e] = make_float2(0.f, 0.f);
+
+  const int steps = 4 * a.iters;
+  int8_t* trace = nullptr;
+  float* trc = nullptr;
+  if (a.mode == MODE_TRACE) {
+    trace = a.tr_signs + (item * steps) * int64_t(C::N);
+    trc = a.tr_c + item * steps;
+  }
+  float2 cs[4];
+  float2 csum_u = make_float2(0.f, 0.f), csum_v = make_float2(0.f, 0.f);
+  auto step = [&](int t, int st, float2 c) {
+    if (t == 0) cs[st] = c;
+    if (trc != nullptr && threadIdx.x == 0) trc[4 * t + st] = (side ? c.y : c.x) * (side ? unscale.y : unscale.x);
+  };
+  for (int t = 0; t < a.iters; ++t) {
+    if (t > 0) applyP(z);  // back to the residual rho
+    int8_t* tr = trace ? trace + int64_t(4 * t) * C::N : nullptr;
+    // two steps on the cube Q_N, accumulating into u (u itself is recovered at the end)
+    float2 c = greedy_step<C, false>(z, vh, red, slot, tr, side);
+    step(t, 0, c);
+    csum_u = cadd(csum_u, c);
+    c = greedy_step<C, false>(z, vh, red, slot, tr ? tr + C::N : nullptr, side);
+    step(t, 1, c);
+    csum_u = cadd(csum_u, c);
+    // two steps on P Q_N, in the z = P rho domain, accumulating into vhat
+    applyP(z);
+    c = greedy_step<C, true>(z, vh, red, slot, tr ? tr + 2 * C::N : nullptr, side);
+    step(t, 2, c);
+    csum_v = cadd(csum_v, c);
+    c = greedy_step<C, true>(z, vh, red, slot, tr ? tr + 3 * C::N : nullptr, side);
+    step(t, 3, c);
+    csum_v = cadd(csum_v, c);
+  }
+
+  // Epilogue.  vhat is consumed first (written out, or clustered into codes) so that it is
+  // not live while u = w - P(z + vhat) is formed: the register peak stays that of the loop.
+  const float qnan = __int_as_float(0x7fc00000);
+  const bool want_r = (a.mode == MODE_DECOMPOSE) && a.r != nullptr;
+  float vmax[2] = {0.f, 0.f};
+  if (a.mode == MODE_QUANTIZE) {
+    float qv[2][4];
+    cluster_factor<C, LLOYD>(vh, cs[2], cs[3], a.lloyd, red, slot, qv);
+    write_codes<C>(vh, qv, lds, a.codes_v, ra, rb, bad_a, bad_b);
+    if (threadIdx.x == 0) store_centers(a.centers, 1, qv, ra, rb, unscale, bad_a, bad_b);
+  } else {
+    int64_t oa = ra, ob = rb;
+    bool wa = true, wb = rb >= 0;
+    if (a.mode == MODE_TRACE) {
+      wa = side == 0;
+      wb = side == 1;
+      oa = ob = item;
     }
+    if (want_r) {  // keep the final z (scaled) in the r buffer until P z is formed below
+      for_each_elem<C>([&](int e, int i) {
+        a.r[ra * C::N + i] = z[e].x;
+        if (rb >= 0) a.r[rb * C::N + i] = z[e].y;
+      });
+    }
+    for_each_elem<C>([&](int e, int i) {
+      if (wa) a.vhat[oa * C::N + i] = bad_a ? qnan : vh[e].x * unscale.x;
+      if (wb) a.vhat[ob * C::N + i] = bad_b ? qnan : vh[e].y * unscale.y;
+    });
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      vmax[0] = fmaxf(vmax[0], fabsf(vh[e].x));
+      vmax[1] = fmaxf(vmax[1], fabsf(vh[e].y));
+    }
+  }
+
+  // u = w - P(z + vhat) (row reloaded from HBM)
+#pragma unroll
+  for (int e = 0; e < C::E; ++e) z[e] = cadd(z[e], vh[e]);
+  applyP(z);
+  sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
+  float2(&u)[C::E] = z;
+
+  if (a.mode == MODE_QUANTIZE) {
+    float qu[2][4];
+    cluster_factor<C, LLOYD>(u, cs[0], cs[1], a.lloyd, red, slot, qu);
+    write_codes<C>(u, qu, lds, a.codes_u, ra, rb, bad_a, bad_b);
+    if (threadIdx.x == 0) store_centers(a.centers, 0, qu, ra, rb, unscale, bad_a, bad_b);
+    return;
+  }
+
+  {
+    int64_t oa = ra, ob = rb;
+    bool wa = true, wb = rb >= 0;
+    if (a.mode == MODE_TRACE) {
+      wa = side == 0;
+      wb = side == 1;
+      oa = ob = item;
+    }
+    for_each_elem<C>([&](int e, int i) {
+      if (wa) a.u[oa * C::N + i] = bad_a ? qnan : u[e].x * unscale.x;
+      if (wb) a.u[ob * C::N + i] = bad_b ? qnan : u[e].y * unscale.y;
+    });
+  }
+  if (a.mode != MODE_DECOMPOSE) return;
+  if (a.bounds != nullptr) {
+    float mx[4] = {0.f, vmax[0], 0.f, vmax[1]};
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      mx[0] = fmaxf(mx[0], fabsf(u[e].x));
+      mx[2] = fmaxf(mx[2], fabsf(u[e].y));
+    }
+    block_max<C::T, 4>(mx, red, slot);
+    if (threadIdx.x == 0) {
+      float* bo = a.bounds + ra * 4;
+      bo[0] = bad_a ? qnan : mx[0] * unscale.x;
+      bo[1] = bad_a ? qnan : mx[1] * unscale.x;
+      bo[2] = bad_a ? qnan : csum_u.x * unscale.x;
+      bo[3] = bad_a ? qnan : csum_v.x * unscale.x;
+      if (rb >= 0) {
+        bo[4] = bad_b ? qnan : mx[2] * unscale.y;
+        bo[5] = bad_b ? qnan : mx[3] * unscale.y;
+        bo[6] = bad_b ? qnan : csum_u.y * unscale.y;
+        bo[7] = bad_b ? qnan : csum_v.y * unscale.y;
+      }
+    }
+  }
+  if (a.cstep != nullptr && threadIdx.x == 0) {
+    float* co = a.cstep + ra * 4;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) co[st] = bad_a ? qnan : cs[st].x * unscale.x;
+    if (rb >= 0) {
+#pragma unroll
+      for (int st = 0; st < 4; ++st) co[4 + st] = bad_b ? qnan : cs[st].y * unscale.y;
+    }
+  }
+  if (want_r) {
+    // r = P z_final (the residual of Alg. 2), from the z saved above
+    __syncthreads();  // the saved z is read back by other threads of the workgroup
+    load_pair_t<C>(z, a.r, C::N, ra, rb);
+    applyP(z);
+    for_each_elem<C>([&](int e, int i) {
+      a.r[ra * C::N + i] = bad_a ? qnan : z[e].x * unscale.x;
+      if (rb >= 0) a.r[rb * C::N + i] = bad_b ? qnan : z[e].y * unscale.y;
+    });
   }
 }
 
@@ -757,7 +1073,7 @@ __global__ __launch_bounds__(C::T) void pair_greedy_kernel(KArgs a, int64_t item
 // MODE_APPLY_P: y = P x.  MODE_RECON: w_hat = u_q + P v_q from codes and centres.
 template <class C>
 __global__ __launch_bounds__(C::T) void pair_pmap_kernel(KArgs a, int64_t item0) {
-  __shared__ float2 lds[C::LDS];
+  __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
   __shared__ float red[2 * C::NW * 32];
   const int64_t item = item0 + blockIdx.x;
   const int64_t ra = 2 * item;
@@ -785,7 +1101,13 @@ __global__ __launch_bounds__(C::T) void pair_pmap_kernel(KArgs a, int64_t item0)
   float2 scale, unscale;
   bool bad_a, bad_b;
   normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
-  apply_P<C>(z, lds, a.tw, a.mid);
+  if constexpr (resident_ok<C>()) {
+    ResRegs<C> rr;
+    resident_load<C>(rr, lds, a.tw, a.mid4);
+    apply_P_res<C>(z, lds, rr);
+  } else {
+    apply_P<C>(z, lds, a.tw, a.mid4);
+  }
   const float qnan = __int_as_float(0x7fc00000);
   const uint8_t* cu = static_cast<const uint8_t*>(a.w);
   for_each_elem<C>([&](int e, int i) {
@@ -823,9 +1145,9 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
 }  // namespace
 
 // Defines the external launcher launch_n<N> for one launch configuration.
-#define KASHIN_DEFINE_SIZE(N, T, ...)                                                        \
+#define KASHIN_DEFINE_SIZE(N, T, W, ...)                                                     \
   hipError_t launch_n##N(const KArgs& a, int64_t grid, hipStream_t stream) {                \
-    return launch_cfg<Cfg<N, T, __VA_ARGS__>>(a, grid, stream);                             \
+    return launch_cfg<Cfg<N, T, W, __VA_ARGS__>>(a, grid, stream);                          \
   }
 
 }  // namespace kashin
