@@ -487,9 +487,25 @@ constexpr int small_tw_total() {
 
 template <class C>
 struct ResRegs {
-  float2 tw[C::R0];         // w_N^(r t), r < R: twiddles of the last pass (index 0 unused)
-  const float4* mid_row;    // this thread's eps factors: entries k = t + r N/R, r < R
+  float2 tw[C::R0];  // w_N^(r t) for r in {1, 2, 3, 4, 8, 12}: the rest are products of two of these
+  float2 f[C::R0];   // eps factors of the fused step for elements k = t + r N/R
 };
+
+// twiddle r of the last pass from the stored powers (R = 16: r = 4a + b, w_r = w_4a * w_b)
+template <class C, int r>
+__device__ __forceinline__ float2 last_tw(const ResRegs<C>& rr) {
+  if constexpr (C::R0 < 16 || r <= 4 || r == 8 || r == 12) {
+    return rr.tw[r];
+  } else {
+    constexpr int hi = r & ~3, lo = r & 3;
+    float2 x = rr.tw[hi];
+    const float2 y = rr.tw[lo];
+    // keep the product inside the loop (it is loop-invariant and would otherwise be hoisted
+    // out and kept live, which is exactly the register cost this avoids)
+    asm volatile("" : "+v"(x.x), "+v"(x.y));
+    return make_float2(x.x * y.x - x.y * y.y, x.x * y.y + x.y * y.x);
+  }
+}
 
 template <class C>
 __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const float2* __restrict__ tw,
@@ -499,11 +515,18 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
   const float4* t4 = reinterpret_cast<const float4*>(tw + tw_offset<C, false>(C::NP - 1) + t * R);
   sfor<0, R / 2>([&](auto hv) {
     constexpr int h = decltype(hv)::value;
-    const float4 q = t4[h];
-    rr.tw[2 * h] = make_float2(q.x, q.y);
-    rr.tw[2 * h + 1] = make_float2(q.z, q.w);
+    constexpr bool keep0 = (R < 16) || (2 * h <= 4 || 2 * h == 8 || 2 * h == 12);
+    constexpr bool keep1 = (R < 16) || (2 * h + 1 <= 4);
+    if constexpr (keep0 || keep1) {
+      const float4 q = t4[h];
+      if constexpr (keep0) rr.tw[2 * h] = make_float2(q.x, q.y);
+      if constexpr (keep1) rr.tw[2 * h + 1] = make_float2(q.z, q.w);
+    }
   });
-  rr.mid_row = mid + t * R;
+  sfor<0, R>([&](auto rv) {
+    const float4 m = mid[t * R + decltype(rv)::value];
+    rr.f[decltype(rv)::value] = make_float2(m.x, m.y);
+  });
   // inner-pass tables, transposed to [r][jm] so that the lanes of a wave (consecutive jm)
   // read consecutive LDS words (the [jm][r] rows of the global layout are 8R bytes apart,
   // which would put every lane of a 16-lane group on the same banks)
@@ -542,6 +565,7 @@ __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) 
   sfor<1, R>([&](auto rv) {
     constexpr int r = decltype(rv)::value;
     a[r] = twmul<INV>(a[r], tb[r * NS]);
+    if constexpr (r % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // few twiddles in flight
   });
   const int idx0 = (t / NS) * NS * R + jm;
   float2* wb = lds + pad(idx0);
@@ -583,16 +607,14 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
   // forward last pass (stride N/R), fused with the eps step and the inverse first pass
   float2 y[R];
   {
-    // eps factors for the fused step, fetched now so their latency overlaps this pass
-    float2 f[R];
-    sfor<0, R>([&](auto rv) {
-      const float4 m = rr.mid_row[decltype(rv)::value];
-      f[decltype(rv)::value] = make_float2(m.x, m.y);
-    });
+    const float2(&f)[R] = rr.f;
     const float2* rb = lds + pad(t);
     sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
     __syncthreads();
-    sfor<1, R>([&](auto rv) { y[decltype(rv)::value] = twmul<false>(y[decltype(rv)::value], rr.tw[decltype(rv)::value]); });
+    sfor<1, R>([&](auto rv) {
+      constexpr int r = decltype(rv)::value;
+      y[r] = twmul<false>(y[r], last_tw<C, r>(rr));
+    });
     dft_pow2<R, false>(y);  // y[q] = Y_{t + q NB}
     float2* wb = lds + pad(t);
     sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NB)] = y[decltype(qv)::value]; });
@@ -607,7 +629,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
       const float2 oth = pb[-q * pad(NB)];
       const float2 v = (fq.y != 0.f) ? oth : own;
       y[q] = make_float2(fq.x * v.x - fq.y * v.y, fq.x * v.y + fq.y * v.x);
-      if constexpr (q % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
+      if constexpr (q % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
     });
     __syncthreads();
   }
@@ -622,7 +644,10 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
   {
     const float2* rb = lds + pad(t);
     sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
-    sfor<1, R>([&](auto rv) { z[decltype(rv)::value] = twmul<true>(z[decltype(rv)::value], rr.tw[decltype(rv)::value]); });
+    sfor<1, R>([&](auto rv) {
+      constexpr int r = decltype(rv)::value;
+      z[r] = twmul<true>(z[r], last_tw<C, r>(rr));
+    });
     dft_pow2<R, true>(z);
   }
 }
