@@ -41,6 +41,27 @@ def hbm_bytes_per_vector(n: int, in_bytes: int) -> int:
     return n * in_bytes + 2 * ((n + 3) // 4) + 32
 
 
+def measured_traffic(launches) -> float | None:
+    """HBM bytes per launch of the dominant kernel from the committed counter summaries
+    (profiles/*.txt, line TRAFFIC_JSON), averaged over `launches` = [(n, workgroups)], or None
+    when no summary was taken on the current kernel sources."""
+    import glob
+
+    from paper_2609_11687_amd.build import source_digest
+
+    digest = source_digest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("TRAFFIC_JSON "):
+                    continue
+                rec = json.loads(line[len("TRAFFIC_JSON "):])
+                keys = [f"{n}/{wg}" for n, wg in launches]
+                if rec.get("digest") == digest and all(k in rec["bytes"] for k in keys):
+                    return sum(rec["bytes"][k] for k in keys) / len(keys)
+    return None
+
+
 def cpu_baseline(wl, rows: int):
     """The float64 oracle on a bounded sample of the workload: the first `rows` rows of the
     first matrix (the dense explicit-cosine matrix is built before timing)."""
@@ -80,7 +101,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--lloyd", type=int, default=0)
-    ap.add_argument("--cpu-rows", type=int, default=256)
+    ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (HBM counter calibration)")
@@ -105,6 +126,7 @@ def main() -> int:
 
     from paper_2609_11687_amd import kashin as K
     from paper_2609_11687_amd import synth
+    from paper_2609_11687_amd.build import source_digest
 
     K.lib()
     wl = synth.WORKLOADS[args.workload]
@@ -186,6 +208,9 @@ def main() -> int:
     dom_flops = sum(spec.rows * counted_flops_per_vector(spec.n, wl.iters) for spec, _ in dom)
     dom_s = sum(ms for _, ms in dom) / 1e3
     achieved = dom_flops / dom_s / 1e12
+    dom_bytes = sum(spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4)
+                    for spec, _ in dom) / len(dom)
+    traffic = measured_traffic([(spec.n, (spec.rows + 1) // 2) for spec, _ in dom])
     result = {
         "metric": METRIC,
         "value": value,
@@ -213,10 +238,13 @@ def main() -> int:
             "peak": PEAK_FP32_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_TFLOPS,
-            "traffic": None,
+            "traffic": traffic,
             "kernel": f"pair_greedy_kernel N={dom_n}",
+            "launches": len(dom),
             "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
+            "algorithmic_bytes_per_launch": dom_bytes,
         },
+        "source_digest": source_digest(),
     }
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle on {args.cpu_rows} rows")

@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -45,6 +46,19 @@ def sources() -> list[str]:
     srcs = [os.path.join(CSRC, "kashin_api.cpp"), os.path.join(CSRC, "kashin_dispatch.hip")]
     srcs += sorted(glob.glob(os.path.join(CSRC, "kashin_n*.hip")))
     return srcs
+
+
+def source_digest() -> str:
+    """SHA-256 over every kernel and interface source (csrc/ and include/): a profile taken on
+    other sources no longer describes the built kernels."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(CSRC, "*")) + glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        if os.path.isfile(f):
+            h.update(os.path.relpath(f, ROOT).encode())
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
 
 
 def _compile(src: str, verbose: bool) -> str:

@@ -1,0 +1,117 @@
+"""Turns rocprofv3 result databases into the short text summaries kept with the measurements.
+
+    python -m paper_2609_11687_amd.profile_summary --trace KT.db \
+        [--fetch F.db --write W.db --copy-fetch CF.db --copy-write CW.db] \
+        --command "..." [--command "..."] > summary.txt
+
+--trace: a `rocprofv3 --kernel-trace --stats` run; per kernel and launch shape it lists the
+number of dispatches and the average duration.  The four counter databases (one
+`--pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` run of the same program, and the same two of a
+plain 256 MiB device copy) give HBM bytes per dispatch: the raw KiB figure times the factor
+that makes the copy's counter read its known size.  The last line of the output,
+`TRAFFIC_JSON {...}`, carries those bytes per (vector length, workgroups) together with the
+digest of the kernel sources they were taken on.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import json
+import re
+import sqlite3
+import sys
+
+from .build import source_digest
+
+COPY_BYTES = 256 << 20  # the calibration copy reads and writes 256 MiB
+
+
+def _short(name: str) -> tuple[str, int]:
+    m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|cluster_kernel|__amd_rocclr_copyBuffer\w*|elementwise_kernel)", name)
+    c = re.search(r"Cfg<(\d+)", name)
+    base = m.group(1) if m else name[:40]
+    if ", true>" in name:
+        base += "[lloyd]"
+    return base, int(c.group(1)) if c else 0
+
+
+def trace_stats(path: str):
+    db = sqlite3.connect(path)
+    rows = db.execute("select name, duration, grid_x, workgroup_x, scratch_size from kernels")
+    agg = collections.defaultdict(list)
+    meta = {}
+    for name, dur, gx, wx, scratch in rows:
+        k, n = _short(name)
+        key = (k, n, gx // max(wx, 1), wx)
+        agg[key].append(dur)
+        meta[key] = scratch
+    return agg, meta
+
+
+def counter_per_dispatch(path: str, counter: str):
+    db = sqlite3.connect(path)
+    rows = db.execute("select kernel_name, grid_size, workgroup_size, value from counters_collection "
+                      "where counter_name = ?", (counter,))
+    agg = collections.defaultdict(list)
+    for name, g, w, v in rows:
+        k, n = _short(name)
+        agg[(k, n, g // max(w, 1), w)].append(v)
+    return {key: sum(v) / len(v) for key, v in agg.items()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-fetch")
+    ap.add_argument("--copy-write")
+    ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--bench-json", help="JSON line printed by the profiled bench run: its source_digest is "
+                                         "recorded (default: the digest of the sources as they are now)")
+    args = ap.parse_args()
+    digest = source_digest()
+    if args.bench_json:
+        with open(args.bench_json) as fh:
+            digest = json.loads(fh.read().strip().splitlines()[-1])["source_digest"]
+    out = []
+    out.append("commands (from the repository root, TMPDIR=/tmp):")
+    out += [f"  {c}" for c in args.command]
+    out.append("")
+    agg, meta = trace_stats(args.trace)
+    out.append("kernel trace (--kernel-trace --stats): average duration per dispatch")
+    out.append(f"  {'kernel':28s} {'N':>6s} {'WGs':>6s} {'threads':>7s} {'calls':>5s} {'avg_us':>10s} "
+               f"{'total_ms':>9s} {'scratch_B':>9s}")
+    for key in sorted(agg, key=lambda k: (-sum(agg[k]), k)):
+        k, n, wg, wx = key
+        v = agg[key]
+        out.append(f"  {k:28s} {n:6d} {wg:6d} {wx:7d} {len(v):5d} {sum(v) / len(v) / 1e3:10.2f} "
+                   f"{sum(v) / 1e6:9.3f} {meta[key]:9d}")
+    traffic = None
+    if args.fetch and args.write and args.copy_fetch and args.copy_write:
+        fetch = counter_per_dispatch(args.fetch, "FETCH_SIZE")
+        write = counter_per_dispatch(args.write, "WRITE_SIZE")
+        cf = [v for (k, *_), v in counter_per_dispatch(args.copy_fetch, "FETCH_SIZE").items() if "copyBuffer" in k]
+        cw = [v for (k, *_), v in counter_per_dispatch(args.copy_write, "WRITE_SIZE").items() if "copyBuffer" in k]
+        f_fac = COPY_BYTES / 1024 / cf[0]
+        w_fac = COPY_BYTES / 1024 / cw[0]
+        out.append("")
+        out.append(f"HBM counters (--pmc FETCH_SIZE, --pmc WRITE_SIZE; KiB per dispatch)")
+        out.append(f"  calibration: 256 MiB device copy reads FETCH_SIZE={cf[0]:.6g} KiB, WRITE_SIZE={cw[0]:.6g} KiB"
+                   f" -> factors {f_fac:.4f} (fetch), {w_fac:.4f} (write)")
+        out.append(f"  {'kernel':28s} {'N':>6s} {'WGs':>6s} {'FETCH_KiB':>11s} {'WRITE_KiB':>11s} {'bytes(cal)':>12s}")
+        traffic = {"digest": digest, "fetch_factor": f_fac, "write_factor": w_fac, "bytes": {}}
+        for key in sorted(set(fetch) & set(write)):
+            k, n, wg, wx = key
+            b = fetch[key] * 1024 * f_fac + write[key] * 1024 * w_fac
+            out.append(f"  {k:28s} {n:6d} {wg:6d} {fetch[key]:11.1f} {write[key]:11.1f} {b:12.4g}")
+            if k == "pair_greedy_kernel":
+                traffic["bytes"][f"{n}/{wg}"] = b
+    print("\n".join(out))
+    if traffic is not None:
+        print("TRAFFIC_JSON " + json.dumps(traffic, sort_keys=True))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
