@@ -17,7 +17,7 @@ namespace kashin {
   X(3072, 192, 3, 16, 16, 4, 3)     \
   X(4096, 256, 3, 16, 16, 16)       \
   X(8192, 512, 2, 16, 16, 16, 2)    \
-  X(11008, 704, 3, 16, 16, 43)      \
+  X(11008, 768, 3, 16, 43, 16)      \
   X(16384, 1024, 4, 16, 16, 16, 4)
 
 #define X(N, ...) hipError_t launch_n##N(const KArgs& a, int64_t grid, hipStream_t stream);

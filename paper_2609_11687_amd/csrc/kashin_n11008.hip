@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(11008, 704, 3, 16, 16, 43)
+KASHIN_DEFINE_SIZE(11008, 768, 3, 16, 43, 16)
 }  // namespace kashin

@@ -466,18 +466,34 @@ __device__ __forceinline__ void apply_P(float2 (&z)[C::E], float2* lds, const fl
 // one, plus Y_{N-k}, which thread N/R - t holds; one LDS exchange brings the partner's
 // values, and the element to use is chosen by the factor itself (f_k.y == 0 exactly when
 // eps_k == eps_{N-k}).
+// An inner pass of odd radix R > R0 whose N/R butterflies are each shared by S = T / (N/R)
+// threads (wave-uniform sub-groups; see split_pass).  Its stride must be R0 so that the
+// forward/inverse first passes can apply its twiddles to their outputs.
+template <class C>
+constexpr bool is_split_pass(int p) {
+  const int R = C::rad[p];
+  return C::NP == 3 && p == 1 && R % 2 == 1 && R > C::R0 && (C::N / R) % 64 == 0 && C::T % (C::N / R) == 0 &&
+         C::T / (C::N / R) <= (R - 1) / 2;
+}
+template <class C>
+constexpr bool has_split_pass() {
+  return C::NP == 3 && is_split_pass<C>(1);
+}
 template <class C>
 constexpr bool resident_ok() {
+  constexpr int R0 = C::R0;
+  if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % 16 == 0))
+    return false;
+  if (has_split_pass<C>()) return C::T >= C::N / R0;
   for (int p = 0; p < C::NP; ++p)
-    if (C::rad[p] != C::R0) return false;
-  return C::NP >= 2 && C::R0 <= 16 && (C::R0 & (C::R0 - 1)) == 0 && C::T == C::N / C::R0 &&
-         (C::N / C::R0) % 16 == 0;
+    if (C::rad[p] != R0) return false;
+  return C::T == C::N / R0;
 }
 // LDS slots (float2) of the inner-pass twiddle tables (passes 1 .. NP-2), after the FFT buffer
 template <class C>
 constexpr int small_tw_offset(int p) {
   int off = 0;
-  for (int q = 1; q < p; ++q) off += ns_fwd<C>(q) * C::R0;
+  for (int q = 1; q < p; ++q) off += ns_fwd<C>(q) * C::rad[q];
   return off;
 }
 template <class C>
@@ -511,8 +527,10 @@ template <class C>
 __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const float2* __restrict__ tw,
                                               const float4* __restrict__ mid) {
   constexpr int R = C::R0;
+  constexpr int NB = C::N / R;
   const int t = threadIdx.x;
-  const float4* t4 = reinterpret_cast<const float4*>(tw + tw_offset<C, false>(C::NP - 1) + t * R);
+  const int tl = (C::T == NB || t < NB) ? t : 0;  // threads past the last butterfly load row 0 (unused)
+  const float4* t4 = reinterpret_cast<const float4*>(tw + tw_offset<C, false>(C::NP - 1) + tl * R);
   sfor<0, R / 2>([&](auto hv) {
     constexpr int h = decltype(hv)::value;
     constexpr bool keep0 = (R < 16) || (2 * h <= 4 || 2 * h == 8 || 2 * h == 12);
@@ -524,7 +542,7 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
     }
   });
   sfor<0, R>([&](auto rv) {
-    const float4 m = mid[t * R + decltype(rv)::value];
+    const float4 m = mid[tl * R + decltype(rv)::value];
     rr.f[decltype(rv)::value] = make_float2(m.x, m.y);
   });
   // inner-pass tables, transposed to [r][jm] so that the lanes of a wave (consecutive jm)
@@ -534,9 +552,10 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
   sfor<1, C::NP - 1>([&](auto pv) {
     constexpr int P = decltype(pv)::value;
     constexpr int NS = ns_fwd<C>(P);
+    constexpr int RP = C::rad[P];
     constexpr int OFF = small_tw_offset<C>(P);
-    for (int i = t; i < NS * R; i += C::T) {
-      const int jm = i / R, r = i % R;
+    for (int i = t; i < NS * RP; i += C::T) {
+      const int jm = i / RP, r = i % RP;
       small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
     }
   });
@@ -578,39 +597,161 @@ __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) 
   __syncthreads();
 }
 
+// Split inner pass: odd radix R, stride NS = R0, NB = N/R butterflies, each shared by the
+// S = T/NB threads t = j + s NB (s is uniform across a wave).  Every sub-group streams the
+// R inputs of butterfly j from LDS once, forming the pair sums and differences
+// a_r +- a_{R-r}, and accumulates only its own share of the (R-1)/2 output pairs (q, R-q);
+// the twiddles were applied by the pass before.  All sub-groups run one code path: their
+// DFT constants come from a table in constant memory at a wave-uniform address (scalar
+// loads into SGPR operands of the FMAs).
+template <class C, int P>
+struct SplitShape {
+  static constexpr int R = C::rad[P];
+  static constexpr int NB = C::N / R;
+  static constexpr int S = C::T / NB;         // threads per butterfly
+  static constexpr int H = (R - 1) / 2;       // output pairs (q, R - q)
+  static constexpr int QP = (H + S - 1) / S;  // output pairs per sub-group
+};
+
+// {cos, sin}(2 pi r q / R) for sub-group s, input pair r = 1..H and output pair
+// q = s QP + 1 + i, at [((s H + r - 1) QP + i) 2] (zero past the last pair).
+template <int R, int S>
+struct SplitCoef {
+  static constexpr int H = (R - 1) / 2;
+  static constexpr int QP = (H + S - 1) / S;
+  float v[S * H * QP * 2];
+};
+template <int R, int S>
+constexpr SplitCoef<R, S> make_split_coef() {
+  SplitCoef<R, S> t{};
+  constexpr int H = SplitCoef<R, S>::H, QP = SplitCoef<R, S>::QP;
+  for (int s = 0; s < S; ++s)
+    for (int r = 1; r <= H; ++r)
+      for (int i = 0; i < QP; ++i) {
+        const int q = s * QP + 1 + i;
+        const int idx = ((s * H + r - 1) * QP + i) * 2;
+        if (q <= H) {
+          t.v[idx] = OddTab<R>::c[(r * q) % R];
+          t.v[idx + 1] = OddTab<R>::s[(r * q) % R];
+        }
+      }
+  return t;
+}
+template <int R, int S>
+__constant__ SplitCoef<R, S> split_coef = make_split_coef<R, S>();
+
+template <class C, int P, bool INV>
+__device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
+  using SS = SplitShape<C, P>;
+  constexpr int R = SS::R;
+  constexpr int NB = SS::NB;
+  constexpr int S = SS::S;
+  constexpr int QP = SS::QP;
+  constexpr int H = SS::H;
+  constexpr int NS = ns_fwd<C>(P);
+  static_assert(NB % 64 == 0 && NS % 16 == 0, "split pass strides");
+  const int s = __builtin_amdgcn_readfirstlane(t / NB);  // uniform across a wave
+  const int j = t - s * NB;
+  const float* __restrict__ cf = split_coef<R, S>.v + s * (H * QP * 2);
+  const float2* rb = lds + pad(j);
+  const float2 x0 = rb[0];
+  float2 re[QP], im[QP];
+  sfor<0, QP>([&](auto iv) {
+    re[decltype(iv)::value] = x0;
+    im[decltype(iv)::value] = make_float2(0.f, 0.f);
+  });
+  float2 sum = x0;
+  sfor<1, H + 1>([&](auto rv) {
+    constexpr int r = decltype(rv)::value;
+    const float2 p = rb[r * pad(NB)], m = rb[(R - r) * pad(NB)];
+    const float2 sp = cadd(p, m), dm = csub(p, m);
+    sum = cadd(sum, sp);
+    const float* cr = cf + (r - 1) * QP * 2;
+    sfor<0, QP>([&](auto iv) {
+      constexpr int i = decltype(iv)::value;
+      const float c = cr[2 * i], sn = cr[2 * i + 1];
+      re[i].x = fmaf(sp.x, c, re[i].x);
+      re[i].y = fmaf(sp.y, c, re[i].y);
+      im[i].x = fmaf(dm.x, sn, im[i].x);
+      im[i].y = fmaf(dm.y, sn, im[i].y);
+    });
+    if constexpr (r % 2 == 0) __builtin_amdgcn_sched_barrier(0);  // few input pairs in flight
+  });
+  __syncthreads();
+  // forward: A_q = re - i im, A_{R-q} = re + i im; the inverse swaps them
+  const int q0 = s * QP + 1;
+  float2* wb = lds + pad((j / NS) * NS * R + (j % NS));
+  sfor<0, QP>([&](auto iv) {
+    constexpr int i = decltype(iv)::value;
+    const float2 minus = make_float2(re[i].x + im[i].y, re[i].y - im[i].x);
+    const float2 plus = make_float2(re[i].x - im[i].y, re[i].y + im[i].x);
+    if (H % QP == 0 || q0 + i <= H) {
+      wb[(q0 + i) * pad(NS)] = INV ? plus : minus;
+      wb[(R - q0 - i) * pad(NS)] = INV ? minus : plus;
+    }
+  });
+  if (s == 0) wb[0] = sum;
+  __syncthreads();
+}
+
 template <class C, int P, bool INV>
 __device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
   if constexpr (P >= 1 && P <= C::NP - 2) {
     // the inverse FFT meets the strides in the same order (R, R^2, ...) as the forward one
-    res_inner_pass<C, P, INV>(lds, t);
+    if constexpr (is_split_pass<C>(P)) split_pass<C, P, INV>(lds, t);
+    else res_inner_pass<C, P, INV>(lds, t);
     res_inner_passes<C, P + 1, INV>(lds, t);
   }
 }
 
-// z <- P z on the resident path.
+// First pass (stride 1) of either direction: a[] -> LDS, element q to t R + q.  When the
+// next pass is a split pass its input twiddles are applied here, to the outputs: element
+// t R0 + q is input r = t / (NB1 / R0) of a butterfly with j mod R0 = q, so its twiddle is
+// entry [r][q] of the LDS copy of that pass's table.
+template <class C, bool INV>
+__device__ __forceinline__ void res_first_pass(float2 (&a)[C::R0], float2* lds, int t) {
+  constexpr int R = C::R0;
+  float2* wb = lds + pad(t * R);
+  if constexpr (has_split_pass<C>()) {
+    constexpr int NB1 = C::N / C::rad[1];
+    static_assert(NB1 % R == 0 && ns_fwd<C>(1) == R, "split pass after the first pass");
+    const float4* tb = reinterpret_cast<const float4*>(lds + C::LDS + small_tw_offset<C>(1) + (t / (NB1 / R)) * R);
+    dft_pow2<R, INV>(a);
+    wb[0] = a[0];
+    sfor<0, R / 2>([&](auto hv) {
+      constexpr int h = decltype(hv)::value;
+      const float4 q = tb[h];
+      if constexpr (h > 0) wb[2 * h] = twmul<INV>(a[2 * h], make_float2(q.x, q.y));
+      wb[2 * h + 1] = twmul<INV>(a[2 * h + 1], make_float2(q.z, q.w));
+    });
+  } else {
+    dft<R, INV>(a, [&](int q, float2 v) { wb[q] = v; });
+  }
+}
+
+// z <- P z on the resident path.  Threads past the last radix-R0 butterfly (T > N/R0, only
+// with a split pass) take part in the split pass and the barriers only.
 template <class C>
 __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, const ResRegs<C>& rr) {
   constexpr int N = C::N;
   constexpr int R = C::R0;
   constexpr int NB = N / R;
-  constexpr int NP = C::NP;
   const int t = opaque(static_cast<int>(threadIdx.x));
-  // forward pass 0 (stride 1): registers -> LDS, element q to t R + q
-  {
+  const bool act = (C::T == NB) || t < NB;
+  // forward pass 0 (stride 1): registers -> LDS
+  if (act) {
     float2 a[R];
     sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = z[decltype(rv)::value]; });
-    float2* wb = lds + pad(t * R);
-    dft<R, false>(a, [&](int q, float2 v) { wb[q] = v; });
-    __syncthreads();
+    res_first_pass<C, false>(a, lds, t);
   }
+  __syncthreads();
   res_inner_passes<C, 1, false>(lds, t);
   // forward last pass (stride N/R), fused with the eps step and the inverse first pass
   float2 y[R];
-  {
-    const float2(&f)[R] = rr.f;
-    const float2* rb = lds + pad(t);
-    sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
-    __syncthreads();
+  const float2* rb = lds + pad(t);
+  if (act) sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+  __syncthreads();
+  if (act) {
     sfor<1, R>([&](auto rv) {
       constexpr int r = decltype(rv)::value;
       y[r] = twmul<false>(y[r], last_tw<C, r>(rr));
@@ -618,9 +759,12 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
     dft_pow2<R, false>(y);  // y[q] = Y_{t + q NB}
     float2* wb = lds + pad(t);
     sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NB)] = y[decltype(qv)::value]; });
-    __syncthreads();
+  }
+  __syncthreads();
+  if (act) {
     // partner values Y_{N - t - q NB} (slot pad(N - t) - q pad(NB); for t = 0, q = 0 the
     // slot just past the buffer is read but never used: k = 0 pairs with itself)
+    const float2(&f)[R] = rr.f;
     const float2* pb = lds + pad(N - t);
     sfor<0, R>([&](auto qv) {
       constexpr int q = decltype(qv)::value;
@@ -631,18 +775,14 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
       y[q] = make_float2(fq.x * v.x - fq.y * v.y, fq.x * v.y + fq.y * v.x);
       if constexpr (q % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
     });
-    __syncthreads();
   }
-  // inverse pass 0 (stride 1): element q to t R + q
-  {
-    float2* wb = lds + pad(t * R);
-    dft<R, true>(y, [&](int q, float2 v) { wb[q] = v; });
-    __syncthreads();
-  }
+  __syncthreads();
+  // inverse pass 0 (stride 1)
+  if (act) res_first_pass<C, true>(y, lds, t);
+  __syncthreads();
   res_inner_passes<C, 1, true>(lds, t);
   // inverse last pass (stride N/R): LDS -> registers
-  {
-    const float2* rb = lds + pad(t);
+  if (act) {
     sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
     sfor<1, R>([&](auto rv) {
       constexpr int r = decltype(rv)::value;

@@ -71,7 +71,8 @@ def test_apply_p_matches_oracle(n):
 
 # ----------------------------------------------------------------------------- Alg. 2 on small batches
 CASES = [(64, 3, "gauss"), (96, 20, "gauss"), (172, 20, "t4"), (256, 1, "gauss"), (512, 20, "gauss"),
-         (768, 30, "outlier"), (1024, 8, "t4"), (2048, 20, "gauss"), (3072, 30, "outlier"), (4096, 30, "t4")]
+         (768, 30, "outlier"), (1024, 8, "t4"), (2048, 20, "gauss"), (3072, 30, "outlier"), (4096, 30, "t4"),
+         (11008, 4, "outlier")]
 
 
 @pytest.mark.parametrize("n,k,dist", CASES)
