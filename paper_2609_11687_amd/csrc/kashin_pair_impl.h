@@ -1057,9 +1057,10 @@ __device__ __forceinline__ void store_centers(float* centers, int f, const float
 // Alg. 2 for a pair of rows.  Only the residual z and the accumulated vhat live in
 // registers across the blocks; after the last block (whose final P is skipped) the
 // first factor is recovered exactly as u = w - P(z + vhat), since w = u + P vhat + P z.
-// LLOYD selects the instance with k-means refinement after the closed form; the
-// closed-form-only instance (a.lloyd == 0) carries none of its registers.
-template <class C, bool LLOYD>
+// QUANT selects the fused quantizer instance (MODE_QUANTIZE), the other one serves
+// MODE_DECOMPOSE and MODE_TRACE; LLOYD (QUANT only) the instance with k-means refinement
+// after the closed form.  Each instance carries only the registers of its own epilogue.
+template <class C, bool LLOYD, bool QUANT>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_greedy_kernel(
     KArgs a, int64_t item0) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
@@ -1067,7 +1068,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   const int64_t item = item0 + blockIdx.x;
   int64_t ra;
   int side = 0;
-  if (a.mode == MODE_TRACE) {
+  if (!QUANT && a.mode == MODE_TRACE) {
     const int64_t row = a.rows[item];
     if (row < 0 || row >= a.m) return;  // uniform: the whole workgroup reads the same entry
     ra = row & ~int64_t(1);
@@ -1097,7 +1098,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   const int steps = 4 * a.iters;
   int8_t* trace = nullptr;
   float* trc = nullptr;
-  if (a.mode == MODE_TRACE) {
+  if (!QUANT && a.mode == MODE_TRACE) {
     trace = a.tr_signs + (item * steps) * int64_t(C::N);
     trc = a.tr_c + item * steps;
   }
@@ -1105,7 +1106,9 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   float2 csum_u = make_float2(0.f, 0.f), csum_v = make_float2(0.f, 0.f);
   auto step = [&](int t, int st, float2 c) {
     if (t == 0) cs[st] = c;
-    if (trc != nullptr && threadIdx.x == 0) trc[4 * t + st] = (side ? c.y : c.x) * (side ? unscale.y : unscale.x);
+    if constexpr (!QUANT) {
+      if (trc != nullptr && threadIdx.x == 0) trc[4 * t + st] = (side ? c.y : c.x) * (side ? unscale.y : unscale.x);
+    }
   };
   for (int t = 0; t < a.iters; ++t) {
     if (t > 0) applyP(z);  // back to the residual rho
@@ -1130,9 +1133,9 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   // Epilogue.  vhat is consumed first (written out, or clustered into codes) so that it is
   // not live while u = w - P(z + vhat) is formed: the register peak stays that of the loop.
   const float qnan = __int_as_float(0x7fc00000);
-  const bool want_r = (a.mode == MODE_DECOMPOSE) && a.r != nullptr;
+  const bool want_r = !QUANT && (a.mode == MODE_DECOMPOSE) && a.r != nullptr;
   float vmax[2] = {0.f, 0.f};
-  if (a.mode == MODE_QUANTIZE) {
+  if constexpr (QUANT) {
     float qv[2][4];
     cluster_factor<C, LLOYD>(vh, cs[2], cs[3], a.lloyd, red, slot, qv);
     write_codes<C>(vh, qv, lds, a.codes_v, ra, rb, bad_a, bad_b);
@@ -1169,7 +1172,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
   float2(&u)[C::E] = z;
 
-  if (a.mode == MODE_QUANTIZE) {
+  if constexpr (QUANT) {
     float qu[2][4];
     cluster_factor<C, LLOYD>(u, cs[0], cs[1], a.lloyd, red, slot, qu);
     write_codes<C>(u, qu, lds, a.codes_u, ra, rb, bad_a, bad_b);
@@ -1295,9 +1298,14 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
   for (int64_t i0 = 0; i0 < grid; i0 += kMaxGrid) {
     const int64_t g = (grid - i0 < kMaxGrid) ? grid - i0 : kMaxGrid;
     if (a.mode == MODE_QUANTIZE && a.lloyd > 0) {
-      hipLaunchKernelGGL((pair_greedy_kernel<C, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
+      hipLaunchKernelGGL((pair_greedy_kernel<C, true, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
+                         i0);
+    } else if (a.mode == MODE_QUANTIZE) {
+      hipLaunchKernelGGL((pair_greedy_kernel<C, false, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
+                         i0);
     } else if (a.mode <= MODE_TRACE) {
-      hipLaunchKernelGGL((pair_greedy_kernel<C, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
+      hipLaunchKernelGGL((pair_greedy_kernel<C, false, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
+                         i0);
     } else {
       hipLaunchKernelGGL(pair_pmap_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
     }

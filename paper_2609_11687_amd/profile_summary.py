@@ -30,8 +30,10 @@ def _short(name: str) -> tuple[str, int]:
     m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|cluster_kernel|__amd_rocclr_copyBuffer\w*|elementwise_kernel)", name)
     c = re.search(r"Cfg<(\d+)", name)
     base = m.group(1) if m else name[:40]
-    if ", true>" in name:
-        base += "[lloyd]"
+    flags = re.search(r">, (true|false), (true|false)>", name)  # pair_greedy_kernel<Cfg, LLOYD, QUANT>
+    if flags:
+        base += ("[quantize" + (",lloyd" if flags.group(1) == "true" else "") + "]"
+                 if flags.group(2) == "true" else "[decompose]")
     return base, int(c.group(1)) if c else 0
 
 
@@ -105,7 +107,7 @@ def main() -> int:
             k, n, wg, wx = key
             b = fetch[key] * 1024 * f_fac + write[key] * 1024 * w_fac
             out.append(f"  {k:28s} {n:6d} {wg:6d} {fetch[key]:11.1f} {write[key]:11.1f} {b:12.4g}")
-            if k == "pair_greedy_kernel":
+            if k.startswith("pair_greedy_kernel[quantize"):
                 traffic["bytes"][f"{n}/{wg}"] = b
     print("\n".join(out))
     if traffic is not None:

@@ -106,3 +106,15 @@ def code_mismatches(codes_gpu, x_ref, q_ref, winf, label=""):
 
 def unpack(packed, n):
     return ref.unpack2bit(packed, n)
+
+
+def assert_centres_close(ce, q, rel=1e-5):
+    """Centres of one factor per row ([-(a+b), -|a-b|, |a-b|, a+b]) against the oracle's.  The
+    inner centre |a-b| cancels when a ~ b, so its error is bounded by the errors of a and b:
+    every centre is compared relative to the row's outer centre a+b."""
+    ce = np.asarray(ce, dtype=np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    scale = np.abs(q).max(axis=1)
+    err = np.abs(ce - q).max(axis=1)
+    bad = err > rel * scale + 1e-30
+    assert not bad.any(), f"centres differ: rows {np.nonzero(bad)[0][:8]}, rel err {(err / np.maximum(scale, 1e-30)).max():.2e}"

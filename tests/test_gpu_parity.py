@@ -178,8 +178,8 @@ def test_codes_against_oracle_decomposition():
     rep = res["rep"]
     qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
     qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
-    np.testing.assert_allclose(ce.cpu().numpy()[:, 0], qu, rtol=1e-5, atol=0)
-    np.testing.assert_allclose(ce.cpu().numpy()[:, 1], qv, rtol=1e-5, atol=0)
+    pu.assert_centres_close(ce.cpu().numpy()[:, 0], qu)
+    pu.assert_centres_close(ce.cpu().numpy()[:, 1], qv)
     mu, tot = pu.code_mismatches(pu.unpack(cu.cpu().numpy(), n), rep["u"], qu, res["winf"], "u")
     mv, _ = pu.code_mismatches(pu.unpack(cv.cpu().numpy(), n), rep["vhat"], qv, res["winf"], "vhat")
     assert mu + mv <= max(1, int(2e-4 * tot))
@@ -288,10 +288,44 @@ def _sample_rows(w, count, rng):
 WL = [("gauss512", None), ("opt125m", 4), ("llama7b", 3), ("pythia7b", 2)]
 
 
+def _check_matrix(key, wl, layer, idx, per_matrix, rng):
+    """Quantise matrix idx of layer `layer` in full (the launch configuration the benchmark
+    times), replay sampled rows (all rows if per_matrix is None) against the oracle: factors,
+    reconstruction, centres and codes.  Returns (code mismatches, codes compared)."""
+    spec = wl.matrices[idx]
+    w = synth.make_matrix(wl, layer, idx)
+    seed = synth.sign_seed(wl, layer, idx)
+    plan = K.kashin_plan(spec.n, seed, wl.iters)
+    dt = torch.float16 if spec.dtype == "f16" else torch.float32
+    wd = pu.to_dev(w).to(dt)
+    cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+    rows = list(range(w.shape[0])) if per_matrix is None else _sample_rows(w, per_matrix, rng)
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, rows, wl.iters)
+    eps = ref.sign_mask(spec.n, seed)
+    w64 = w[rows].astype(np.float64)
+    res = pu.replay_parity(w64, eps, wl.iters, signs, u_tr, v_tr)
+    _say(f"{key}/L{layer}/{spec.name} N={spec.n} rows={len(rows)}: du={res['du'].max():.2e} "
+         f"dv={res['dv'].max():.2e} rec={res['rec'].max():.2e} direct ok={res['direct_frac_ok']:.2f}")
+    pu.assert_replay_ok(res, f"{key}/L{layer}/{spec.name}")
+    rep = res["rep"]
+    qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
+    qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+    ce_s = ce.cpu().numpy()[rows]
+    pu.assert_centres_close(ce_s[:, 0], qu)
+    pu.assert_centres_close(ce_s[:, 1], qv)
+    codes_u = pu.unpack(cu.cpu().numpy()[rows], spec.n)
+    codes_v = pu.unpack(cv.cpu().numpy()[rows], spec.n)
+    mu, tot = pu.code_mismatches(codes_u, rep["u"], qu, res["winf"], "u")
+    mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat")
+    # every row of the matrix got finite centres
+    assert np.isfinite(ce.cpu().numpy()).all()
+    del plan
+    return mu + mv, 2 * tot
+
+
 @pytest.mark.parametrize("key,per_matrix", WL)
 def test_workload_sampled_rows(key, per_matrix):
-    """Every matrix of the workload quantised in full (the launch configuration the benchmark
-    times); sampled rows replayed against the oracle (factors, reconstruction, codes)."""
+    """Every matrix of the workload (first layer) quantised in full; sampled rows replayed."""
     wl = synth.WORKLOADS[key]
     rng = np.random.default_rng(11)
     total_m = total_codes = 0
@@ -300,34 +334,24 @@ def test_workload_sampled_rows(key, per_matrix):
             continue  # same shapes as q_proj / gate_proj; keeps the test within its time budget
         if key == "pythia7b" and spec.name in ("qkv_1", "qkv_2", "dense"):
             continue
-        w = synth.make_matrix(wl, 0, idx)
-        seed = synth.sign_seed(wl, 0, idx)
-        plan = K.kashin_plan(spec.n, seed, wl.iters)
-        dt = torch.float16 if spec.dtype == "f16" else torch.float32
-        wd = pu.to_dev(w).to(dt)
-        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
-        rows = list(range(w.shape[0])) if per_matrix is None else _sample_rows(w, per_matrix, rng)
-        signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, rows, wl.iters)
-        eps = ref.sign_mask(spec.n, seed)
-        w64 = w[rows].astype(np.float64)
-        res = pu.replay_parity(w64, eps, wl.iters, signs, u_tr, v_tr)
-        _say(f"{key}/{spec.name} N={spec.n} rows={len(rows)}: du={res['du'].max():.2e} "
-             f"dv={res['dv'].max():.2e} rec={res['rec'].max():.2e} direct ok={res['direct_frac_ok']:.2f}")
-        pu.assert_replay_ok(res, f"{key}/{spec.name}")
-        rep = res["rep"]
-        qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
-        qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
-        ce_s = ce.cpu().numpy()[rows]
-        np.testing.assert_allclose(ce_s[:, 0], qu, rtol=1e-5)
-        np.testing.assert_allclose(ce_s[:, 1], qv, rtol=1e-5)
-        codes_u = pu.unpack(cu.cpu().numpy()[rows], spec.n)
-        codes_v = pu.unpack(cv.cpu().numpy()[rows], spec.n)
-        mu, tot = pu.code_mismatches(codes_u, rep["u"], qu, res["winf"], "u")
-        mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat")
-        total_m += mu + mv
-        total_codes += 2 * tot
-        # every row of the matrix got finite centres
-        assert np.isfinite(ce.cpu().numpy()).all()
-        del plan
+        mm, tot = _check_matrix(key, wl, 0, idx, per_matrix, rng)
+        total_m += mm
+        total_codes += tot
     _say(f"{key}: code mismatches {total_m} of {total_codes}")
+    assert total_m <= max(1, int(1e-4 * total_codes))
+
+
+def test_stack_first_and_last_layer():
+    """The 32-layer stack (Student-t(3), outlier columns x50, k = 40): q_proj and down_proj of
+    the first and the last layer quantised in full, two sampled rows each replayed."""
+    wl = synth.WORKLOADS["llama7b_stack"]
+    rng = np.random.default_rng(12)
+    names = [s.name for s in wl.matrices]
+    total_m = total_codes = 0
+    for layer in (0, wl.layers - 1):
+        for name in ("q_proj", "down_proj"):
+            mm, tot = _check_matrix("llama7b_stack", wl, layer, names.index(name), 2, rng)
+            total_m += mm
+            total_codes += tot
+    _say(f"llama7b_stack: code mismatches {total_m} of {total_codes}")
     assert total_m <= max(1, int(1e-4 * total_codes))
