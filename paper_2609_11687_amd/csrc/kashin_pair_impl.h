@@ -54,60 +54,78 @@ constexpr int bitrev(int x, int bits) {
   return r;
 }
 
-struct Pow2Tab {  // cos / sin (2 pi m / 16)
-  static constexpr float c[16] = {1.0f, 0.923879533f, 0.707106781f, 0.382683432f, 0.0f, -0.382683432f,
-                                  -0.707106781f, -0.923879533f, -1.0f, -0.923879533f, -0.707106781f,
-                                  -0.382683432f, 0.0f, 0.382683432f, 0.707106781f, 0.923879533f};
-  static constexpr float s[16] = {0.0f, 0.382683432f, 0.707106781f, 0.923879533f, 1.0f, 0.923879533f,
-                                  0.707106781f, 0.382683432f, 0.0f, -0.382683432f, -0.707106781f,
-                                  -0.923879533f, -1.0f, -0.923879533f, -0.707106781f, -0.382683432f};
-};
-
 __device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
 
-// d * w16^K (forward, w16 = exp(-2 pi i / 16)) or d * w16^-K (inverse), K a compile-time constant.
+// cos / sin (2 pi m / 16) in double, for compile-time constants
+struct W16 {
+  static constexpr double C1 = 0.92387953251128674;  // cos(pi / 8)
+  static constexpr double S1 = 0.38268343236508978;  // sin(pi / 8)
+  static constexpr double H = 0.70710678118654752;   // sqrt(1 / 2)
+  static constexpr double c[16] = {1, C1, H, S1, 0, -S1, -H, -C1, -1, -C1, -H, -S1, 0, S1, H, C1};
+  static constexpr double s[16] = {0, S1, H, C1, 1, C1, H, S1, 0, -S1, -H, -C1, -1, -C1, -H, -S1};
+};
+constexpr double cabs_d(double v) { return v < 0 ? -v : v; }
+
+// Radix-2 butterfly with a compile-time twiddle w = w16^K (forward, w16 = exp(-2 pi i / 16);
+// the inverse uses w16^-K): (x, y) <- (x + w y, x - w y).  A general twiddle is applied as
+// w y = m p with p = (w / m) y, m whichever of Re w, Im w is larger in magnitude: p takes
+// two FMAs with the ratio t = Im w / Re w or Re w / Im w (|t| <= 1), and x +- m p four more,
+// six instructions instead of a complex product followed by four additions.
 template <int K, bool INV>
-__device__ __forceinline__ float2 tw16(float2 d) {
+__device__ __forceinline__ void bfly(float2& x, float2& y) {
   constexpr int k = K & 15;
+  const float2 a = x;
   if constexpr (k == 0) {
-    return d;
+    x = cadd(a, y);
+    y = csub(a, y);
   } else if constexpr (k == 8) {
-    return make_float2(-d.x, -d.y);
-  } else if constexpr (k == 4) {
-    if constexpr (INV) return make_float2(-d.y, d.x);
-    else return make_float2(d.y, -d.x);
-  } else if constexpr (k == 12) {
-    if constexpr (INV) return make_float2(d.y, -d.x);
-    else return make_float2(-d.y, d.x);
+    x = csub(a, y);
+    y = cadd(a, y);
+  } else if constexpr (k == 4 || k == 12) {
+    // w = (0, wi), wi = +-1: w y = (-wi y.y, wi y.x)
+    constexpr float wi = static_cast<float>(INV ? W16::s[k] : -W16::s[k]);
+    const float2 wy = make_float2(-wi * y.y, wi * y.x);
+    x = cadd(a, wy);
+    y = csub(a, wy);
   } else {
-    constexpr float c = Pow2Tab::c[k];
-    constexpr float s = INV ? -Pow2Tab::s[k] : Pow2Tab::s[k];
-    return make_float2(fmaf(d.x, c, d.y * s), fmaf(d.y, c, -(d.x * s)));
+    constexpr double wr = W16::c[k];
+    constexpr double wi = INV ? W16::s[k] : -W16::s[k];
+    float2 p;
+    float m;
+    if constexpr (cabs_d(wr) >= cabs_d(wi)) {
+      constexpr float t = static_cast<float>(wi / wr);
+      m = static_cast<float>(wr);
+      p = make_float2(fmaf(-t, y.y, y.x), fmaf(t, y.x, y.y));  // (w / wr) y
+    } else {
+      constexpr float t = static_cast<float>(wr / wi);
+      m = static_cast<float>(wi);
+      p = make_float2(fmaf(t, y.x, -y.y), fmaf(t, y.y, y.x));  // (w / wi) y
+    }
+    x = make_float2(fmaf(m, p.x, a.x), fmaf(m, p.y, a.y));
+    y = make_float2(fmaf(-m, p.x, a.x), fmaf(-m, p.y, a.y));
   }
 }
 
-// In-register DFT of a power-of-two length R <= 16 (radix-2 decimation in frequency,
-// output reordered to natural order at compile time).
+// In-register DFT of a power-of-two length R <= 16: radix-2 decimation in time on the
+// bit-reversed input (a compile-time renaming), so every twiddle multiplies the second
+// operand of a butterfly and fuses with it; output in natural order.
 template <int R, bool INV>
 __device__ __forceinline__ void dft_pow2(float2 (&a)[R]) {
   constexpr int L = ilog2(R);
-  sfor<0, L>([&](auto lv) {
-    constexpr int len = R >> decltype(lv)::value;
+  float2 b[R];
+  sfor<0, R>([&](auto iv) { b[decltype(iv)::value] = a[bitrev(decltype(iv)::value, L)]; });
+  sfor<1, L + 1>([&](auto sv) {
+    constexpr int len = 1 << decltype(sv)::value;
     constexpr int half = len >> 1;
-    sfor<0, R / len>([&](auto sv) {
+    sfor<0, R / len>([&](auto bv) {
       sfor<0, half>([&](auto jv) {
-        constexpr int i0 = decltype(sv)::value * len + decltype(jv)::value;
-        constexpr int i1 = i0 + half;
-        const float2 x = a[i0], y = a[i1];
-        a[i0] = cadd(x, y);
-        a[i1] = tw16<decltype(jv)::value * (16 / len), INV>(csub(x, y));
+        constexpr int i0 = decltype(bv)::value * len + decltype(jv)::value;
+        bfly<decltype(jv)::value * (16 / len), INV>(b[i0], b[i0 + half]);
       });
     });
   });
-  float2 t[R];
-  sfor<0, R>([&](auto iv) { t[decltype(iv)::value] = a[bitrev(decltype(iv)::value, L)]; });
-  sfor<0, R>([&](auto iv) { a[decltype(iv)::value] = t[decltype(iv)::value]; });
+  sfor<0, R>([&](auto iv) { a[decltype(iv)::value] = b[decltype(iv)::value]; });
 }
 
 // In-register DFT of an odd length R, directly from its definition, pairing j with R-j
@@ -514,12 +532,22 @@ __device__ __forceinline__ float2 last_tw(const ResRegs<C>& rr) {
     return rr.tw[r];
   } else {
     constexpr int hi = r & ~3, lo = r & 3;
-    float2 x = rr.tw[hi];
-    const float2 y = rr.tw[lo];
-    // keep the product inside the loop (it is loop-invariant and would otherwise be hoisted
-    // out and kept live, which is exactly the register cost this avoids)
-    asm volatile("" : "+v"(x.x), "+v"(x.y));
+    const float2 x = rr.tw[hi], y = rr.tw[lo];
     return make_float2(x.x * y.x - x.y * y.y, x.x * y.y + x.y * y.x);
+  }
+}
+
+// Before each last pass: declare the stored powers modified (in place, no instruction), so
+// the products formed from them are neither hoisted out of the block loop nor shared between
+// the two last passes of one application of P, either of which would keep nine more complex
+// values live.
+template <class C>
+__device__ __forceinline__ void launder_powers(ResRegs<C>& rr) {
+  if constexpr (C::R0 == 16) {
+    asm volatile(""
+                 : "+v"(rr.tw[1].x), "+v"(rr.tw[1].y), "+v"(rr.tw[2].x), "+v"(rr.tw[2].y), "+v"(rr.tw[3].x),
+                   "+v"(rr.tw[3].y), "+v"(rr.tw[4].x), "+v"(rr.tw[4].y), "+v"(rr.tw[8].x), "+v"(rr.tw[8].y),
+                   "+v"(rr.tw[12].x), "+v"(rr.tw[12].y));
   }
 }
 
@@ -732,7 +760,7 @@ __device__ __forceinline__ void res_first_pass(float2 (&a)[C::R0], float2* lds, 
 // z <- P z on the resident path.  Threads past the last radix-R0 butterfly (T > N/R0, only
 // with a split pass) take part in the split pass and the barriers only.
 template <class C>
-__device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, const ResRegs<C>& rr) {
+__device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResRegs<C>& rr) {
   constexpr int N = C::N;
   constexpr int R = C::R0;
   constexpr int NB = N / R;
@@ -751,6 +779,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
   const float2* rb = lds + pad(t);
   if (act) sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
   __syncthreads();
+  launder_powers<C>(rr);
   if (act) {
     sfor<1, R>([&](auto rv) {
       constexpr int r = decltype(rv)::value;
@@ -782,6 +811,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, cons
   __syncthreads();
   res_inner_passes<C, 1, true>(lds, t);
   // inverse last pass (stride N/R): LDS -> registers
+  launder_powers<C>(rr);
   if (act) {
     sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
     sfor<1, R>([&](auto rv) {
