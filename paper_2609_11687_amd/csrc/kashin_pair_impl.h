@@ -128,6 +128,44 @@ __device__ __forceinline__ void dft_pow2(float2 (&a)[R]) {
   sfor<0, R>([&](auto iv) { a[decltype(iv)::value] = b[decltype(iv)::value]; });
 }
 
+// DFT of the twiddled inputs a_r tw(r) (tw(0) = 1; conjugated twiddles on the inverse).
+// The first DIT stage pairs a_r with a_{r+R/2} (r = bitrev of the pair index): with
+// x = a_r tw(r) and w = tw(r + R/2) it forms X = x + w a_{r+R/2} in four FMAs and the other
+// output as 2x - X, so the second twiddle costs no separate complex product.
+template <int R, bool INV, class TW>
+__device__ __forceinline__ void dft_pow2_tw(float2 (&a)[R], TW&& tw) {
+  constexpr int L = ilog2(R);
+  constexpr int H = R / 2;
+  float2 b[R];
+  sfor<0, H>([&](auto mv) {
+    constexpr int m = decltype(mv)::value;
+    constexpr int r = bitrev(m, L - 1);
+    float2 x = a[r];
+    if constexpr (r > 0) {
+      const float2 t = tw(std::integral_constant<int, r>{});
+      x = INV ? make_float2(x.x * t.x + x.y * t.y, x.y * t.x - x.x * t.y)
+              : make_float2(x.x * t.x - x.y * t.y, x.x * t.y + x.y * t.x);
+    }
+    const float2 w = tw(std::integral_constant<int, r + H>{});
+    const float2 y = a[r + H];
+    const float wy = INV ? -w.y : w.y;
+    const float2 X = make_float2(fmaf(w.x, y.x, fmaf(-wy, y.y, x.x)), fmaf(w.x, y.y, fmaf(wy, y.x, x.y)));
+    b[2 * m] = X;
+    b[2 * m + 1] = make_float2(fmaf(2.f, x.x, -X.x), fmaf(2.f, x.y, -X.y));
+  });
+  sfor<2, L + 1>([&](auto sv) {
+    constexpr int len = 1 << decltype(sv)::value;
+    constexpr int half = len >> 1;
+    sfor<0, R / len>([&](auto bv) {
+      sfor<0, half>([&](auto jv) {
+        constexpr int i0 = decltype(bv)::value * len + decltype(jv)::value;
+        bfly<decltype(jv)::value * (16 / len), INV>(b[i0], b[i0 + half]);
+      });
+    });
+  });
+  sfor<0, R>([&](auto iv) { a[decltype(iv)::value] = b[decltype(iv)::value]; });
+}
+
 // In-register DFT of an odd length R, directly from its definition, pairing j with R-j
 // so each constant multiplies a sum or a difference.  The sums and differences overwrite
 // the inputs in place (a[j] <- a[j] + a[R-j], a[R-j] <- a[j] - a[R-j]) and outputs are
@@ -609,18 +647,14 @@ __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) 
   __syncthreads();
   const int jm = t % NS;
   const float2* tb = lds + C::LDS + small_tw_offset<C>(P) + jm;  // table [r][jm]
-  sfor<1, R>([&](auto rv) {
-    constexpr int r = decltype(rv)::value;
-    a[r] = twmul<INV>(a[r], tb[r * NS]);
-    if constexpr (r % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // few twiddles in flight
-  });
+  dft_pow2_tw<R, INV>(a, [&](auto rv) { return tb[decltype(rv)::value * NS]; });
   const int idx0 = (t / NS) * NS * R + jm;
   float2* wb = lds + pad(idx0);
   static_assert(NS % 16 == 0 || (NS * R) % 16 == 0, "inner pass stride");
   if constexpr (NS % 16 == 0) {
-    dft<R, INV>(a, [&](int q, float2 v) { wb[q * pad(NS)] = v; });
+    sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NS)] = a[decltype(qv)::value]; });
   } else {
-    dft<R, INV>(a, [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+    sfor<0, R>([&](auto qv) { lds[pad(idx0 + decltype(qv)::value * NS)] = a[decltype(qv)::value]; });
   }
   __syncthreads();
 }
@@ -781,11 +815,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   __syncthreads();
   launder_powers<C>(rr);
   if (act) {
-    sfor<1, R>([&](auto rv) {
-      constexpr int r = decltype(rv)::value;
-      y[r] = twmul<false>(y[r], last_tw<C, r>(rr));
-    });
-    dft_pow2<R, false>(y);  // y[q] = Y_{t + q NB}
+    dft_pow2_tw<R, false>(y, [&](auto rv) { return last_tw<C, decltype(rv)::value>(rr); });  // y[q] = Y_{t + q NB}
     float2* wb = lds + pad(t);
     sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NB)] = y[decltype(qv)::value]; });
   }
@@ -814,11 +844,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   launder_powers<C>(rr);
   if (act) {
     sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
-    sfor<1, R>([&](auto rv) {
-      constexpr int r = decltype(rv)::value;
-      z[r] = twmul<true>(z[r], last_tw<C, r>(rr));
-    });
-    dft_pow2<R, true>(z);
+    dft_pow2_tw<R, true>(z, [&](auto rv) { return last_tw<C, decltype(rv)::value>(rr); });
   }
 }
 
