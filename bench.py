@@ -1,12 +1,15 @@
 #!/usr/bin/env python3
-"""Throughput of the fused Kashin-DCT quantizer (decompose + four-peak 2-bit clustering +
-packing) on one MI355X.
+"""Throughput of the Kashin-DCT hot path on one MI355X.  Prints one JSON line.
 
-One step = kashin_quantize over every matrix of the workload (default: one
-Llama-2-7B-shaped decoder layer, fp16-stored, 30 blocks of Alg. 2, closed-form
-centres), inputs already resident in HBM.  Prints one JSON line.
+    python bench.py [--steps K] [--warmup W] [--workload llama7b] [--lloyd 0] [--op quantize]
 
-    python bench.py [--steps K] [--warmup W] [--workload llama7b] [--lloyd 0]
+--op quantize (default): one step = kashin_quantize (decompose with Alg. 2 + four-peak 2-bit
+  clustering + packing) over every matrix of the workload (default: one Llama-2-7B-shaped decoder
+  layer, fp16-stored, 30 blocks, closed-form centres), inputs already resident in HBM.
+--op apply_p: one step = y = P x (kashin_apply_p) over --act-rows fp32 activation rows for each
+  input width N of the workload (the inference-side product of App. C).
+--op reconstruct: one step = w_hat = u_q + P v_q (kashin_reconstruct) from the codes and centres
+  of every matrix of the workload (quantized once, untimed).
 """
 from __future__ import annotations
 
@@ -16,24 +19,34 @@ import math
 import os
 import sys
 import time
+from dataclasses import dataclass
+from typing import Callable
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "weight vectors decomposed/s (N=4096, fixed iters); % of HBM / FP32 VALU roofline"
+METRIC_APPLY_P = "activation rows transformed/s (y = P x, fp32); % of HBM roofline"
+METRIC_RECON = "weight rows reconstructed/s (w_hat = u_q + P v_q from 2+2-bit codes, fp32 out); % of HBM roofline"
 PEAK_FP32_TFLOPS = 157.3   # MI355X published FP32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
 PEAK_HBM_GBPS = 8000.0     # MI355X published HBM3E bandwidth
+PMAP_GRID = 2048           # workgroups of a P-only launch (the library's cap; each walks several pairs)
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def transform_flops(n: int) -> float:
+    """Counted flops of one length-n DCT-II or DCT-III: 2.5 n log2 n."""
+    return 2.5 * n * math.log2(n)
+
+
 def counted_flops_per_vector(n: int, k: int) -> float:
     """Algorithmic count: 4k - 2 transforms (two P per block, the last one not needed for the
     factors), each 2.5 N log2 N flops."""
-    return (4 * k - 2) * 2.5 * n * math.log2(n)
+    return (4 * k - 2) * transform_flops(n)
 
 
 def hbm_bytes_per_vector(n: int, in_bytes: int) -> int:
@@ -41,25 +54,42 @@ def hbm_bytes_per_vector(n: int, in_bytes: int) -> int:
     return n * in_bytes + 2 * ((n + 3) // 4) + 32
 
 
-def measured_traffic(launches) -> float | None:
-    """HBM bytes per launch of the dominant kernel from the committed counter summaries
-    (profiles/*.txt, line TRAFFIC_JSON), averaged over `launches` = [(n, workgroups)], or None
-    when no summary was taken on the current kernel sources."""
-    import glob
+@dataclass
+class Launch:
+    n: int
+    rows: int
+    flops: float          # counted flops of the launch
+    nbytes: float         # algorithmic HBM bytes of the launch
+    run: Callable         # run(stream)
 
+
+def measured_traffic(op: str, workload: str, kernel: str, launches) -> float | None:
+    """HBM bytes per launch of the dominant kernel from the committed counter summary of this
+    op and workload (profiles/<kernel>__<op>_<workload>.txt, line TRAFFIC_JSON), averaged over
+    `launches` = [(n, workgroups)], or None when that summary was not taken on the current
+    kernel sources."""
     from paper_2609_11687_amd.build import source_digest
 
-    digest = source_digest()
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
-        with open(path) as fh:
-            for line in fh:
-                if not line.startswith("TRAFFIC_JSON "):
-                    continue
+    path = os.path.join(ROOT, "profiles", f"{kernel.split('[')[0]}__{op}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("TRAFFIC_JSON "):
                 rec = json.loads(line[len("TRAFFIC_JSON "):])
-                keys = [f"{n}/{wg}" for n, wg in launches]
-                if rec.get("digest") == digest and all(k in rec["bytes"] for k in keys):
+                keys = [f"{kernel}|{n}/{wg}" for n, wg in launches]
+                if rec.get("digest") == source_digest() and all(k in rec["bytes"] for k in keys):
                     return sum(rec["bytes"][k] for k in keys) / len(keys)
     return None
+
+
+def _blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return os.cpu_count() or 1
 
 
 def cpu_baseline(wl, rows: int):
@@ -74,24 +104,93 @@ def cpu_baseline(wl, rows: int):
     w = synth.make_matrix(wl, 0, 0, rows=slice(0, rows)).astype(np.float64)
     eps = ref.sign_mask(spec.n, synth.sign_seed(wl, 0, 0))
     ref.dct2_matrix(spec.n)
-    try:
-        from threadpoolctl import threadpool_info
-
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
     t0 = time.perf_counter()
     ref.quantize(w, eps, wl.iters, 0)
     dt = time.perf_counter() - t0
     return {
         "value": rows / dt,
         "unit": "vectors/s",
-        "cores": int(cores),
+        "cores": int(_blas_threads()),
         "kind": "oracle",
         "sample": f"{rows} rows of {spec.name} ({spec.rows}x{spec.n}), k={wl.iters}, float64 literal Alg. 2 "
                   f"with a dense P (4 GEMMs per block) + closed-form clustering + packing; "
                   f"{dt:.1f} s; cosine-matrix construction excluded",
     }
+
+
+def cpu_baseline_apply_p(n: int, rows: int):
+    """The oracle's P (two dense float64 GEMMs with the explicit cosine matrix) on `rows` rows."""
+    import numpy as np
+
+    import oracle.kashin_ref as ref
+
+    x = np.random.default_rng(0).standard_normal((rows, n))
+    eps = ref.sign_mask(n, 0)
+    ref.dct2_matrix(n)
+    t0 = time.perf_counter()
+    ref.apply_p(x, eps)
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "rows/s", "cores": int(_blas_threads()), "kind": "oracle",
+            "sample": f"{rows} Gaussian rows of width {n}, float64 dense P; {dt:.1f} s; "
+                      f"cosine-matrix construction excluded"}
+
+
+def time_launches(launches, steps: int, warmup: int, stream):
+    """Whole-step time (no events inside the step) and the average duration of every launch
+    (HIP events recorded on the launch stream around each one)."""
+    import torch
+
+    def step(events=None):
+        for i, l in enumerate(launches):
+            if events is not None:
+                events[i][0].record(stream)
+            l.run(stream)
+            if events is not None:
+                events[i][1].record(stream)
+
+    log(f"warmup {warmup} steps")
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"timing {steps} steps")
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / steps
+    launch_ms = [0.0] * len(launches)
+    for _ in range(steps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
+        step(ev)
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(ev):
+            launch_ms[i] += a.elapsed_time(b) / steps
+    return ms_per_step, launch_ms
+
+
+def per_n_figures(launches, launch_ms):
+    by_n = {}
+    for l, ms in zip(launches, launch_ms):
+        d = by_n.setdefault(l.n, {"vectors": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        d["vectors"] += l.rows
+        d["ms"] += ms
+        d["flops"] += l.flops
+        d["bytes"] += l.nbytes
+    out = {}
+    for n, d in sorted(by_n.items()):
+        s = d["ms"] / 1e3
+        out[str(n)] = {
+            "vectors_per_s": d["vectors"] / s,
+            "counted_tflops": d["flops"] / s / 1e12,
+            "valu_frac": d["flops"] / s / 1e12 / PEAK_FP32_TFLOPS,
+            "hbm_gbps": d["bytes"] / s / 1e9,
+            "hbm_frac": d["bytes"] / s / 1e9 / PEAK_HBM_GBPS,
+            "ms_per_step": d["ms"],
+        }
+    return by_n, out
 
 
 def main() -> int:
@@ -100,7 +199,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
+    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct"), default="quantize")
     ap.add_argument("--lloyd", type=int, default=0)
+    ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -112,7 +213,6 @@ def main() -> int:
               "with no communication; only --gpus 1 is supported in this build.", file=sys.stderr)
         return 2
 
-    import numpy as np
     import torch
 
     if args.copy_calibration:
@@ -131,90 +231,100 @@ def main() -> int:
     K.lib()
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
-    mats = []
-    for layer in range(wl.layers):
-        for idx, spec in enumerate(wl.matrices):
-            log(f"generating {args.workload} layer {layer} {spec.name} {spec.rows}x{spec.n}")
-            w = synth.make_matrix(wl, layer, idx)
-            dt = torch.float16 if spec.dtype == "f16" else torch.float32
-            wd = torch.from_numpy(w).to(dev).to(dt)
-            del w
-            plan = K.kashin_plan(spec.n, synth.sign_seed(wl, layer, idx), wl.iters)
-            nb = (spec.n + 3) // 4
-            cu = torch.empty((spec.rows, nb), dtype=torch.uint8, device=dev)
-            cv = torch.empty_like(cu)
-            ce = torch.empty((spec.rows, 2, 4), dtype=torch.float32, device=dev)
-            mats.append((spec, wd, plan, cu, cv, ce))
     stream = torch.cuda.current_stream()
+    launches: list[Launch] = []
+    keep = []  # device buffers and plans referenced by the launches
 
-    def step(events=None):
-        for i, (spec, wd, plan, cu, cv, ce) in enumerate(mats):
-            if events is not None:
-                events[i][0].record(stream)
-            K.kashin_quantize(plan, wd, args.lloyd, cu, cv, ce, stream)
-            if events is not None:
-                events[i][1].record(stream)
-
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
+    if args.op in ("quantize", "reconstruct"):
+        for layer in range(wl.layers):
+            for idx, spec in enumerate(wl.matrices):
+                log(f"generating {args.workload} layer {layer} {spec.name} {spec.rows}x{spec.n}")
+                w = synth.make_matrix(wl, layer, idx)
+                dt = torch.float16 if spec.dtype == "f16" else torch.float32
+                wd = torch.from_numpy(w).to(dev).to(dt)
+                del w
+                plan = K.kashin_plan(spec.n, synth.sign_seed(wl, layer, idx), wl.iters)
+                nb = (spec.n + 3) // 4
+                cu = torch.empty((spec.rows, nb), dtype=torch.uint8, device=dev)
+                cv = torch.empty_like(cu)
+                ce = torch.empty((spec.rows, 2, 4), dtype=torch.float32, device=dev)
+                if args.op == "quantize":
+                    keep.append((plan, wd, cu, cv, ce))
+                    launches.append(Launch(
+                        spec.n, spec.rows, spec.rows * counted_flops_per_vector(spec.n, wl.iters),
+                        spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4),
+                        lambda s, a=(plan, wd, cu, cv, ce): K.kashin_quantize(a[0], a[1], args.lloyd, a[2], a[3],
+                                                                              a[4], s)))
+                else:
+                    K.kashin_quantize(plan, wd, args.lloyd, cu, cv, ce, stream)
+                    torch.cuda.synchronize()
+                    del wd
+                    wh = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
+                    keep.append((plan, cu, cv, ce, wh))
+                    launches.append(Launch(
+                        spec.n, spec.rows, spec.rows * 2 * transform_flops(spec.n),
+                        spec.rows * (2 * nb + 32 + 4 * spec.n),
+                        lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s)))
+    else:
+        g = torch.Generator(device=dev).manual_seed(0)
+        for n in sorted({spec.n for spec in wl.matrices}):
+            log(f"activation rows {args.act_rows}x{n}")
+            x = torch.randn((args.act_rows, n), dtype=torch.float32, device=dev, generator=g)
+            y = torch.empty_like(x)
+            plan = K.kashin_plan(n, 0, 1)
+            keep.append((plan, x, y))
+            launches.append(Launch(n, args.act_rows, args.act_rows * 2 * transform_flops(n), args.act_rows * 8 * n,
+                                   lambda s, a=(plan, x, y): K.kashin_apply_p(a[0], a[1], a[2], s)))
     torch.cuda.synchronize()
 
-    # whole-step timing (no per-launch events inside)
-    log(f"timing {args.steps} steps")
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for _ in range(args.steps):
-        step()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_total = t0.elapsed_time(t1)
-    ms_per_step = ms_total / args.steps
+    ms_per_step, launch_ms = time_launches(launches, args.steps, args.warmup, stream)
+    total_vectors = sum(l.rows for l in launches)
+    by_n, per_n = per_n_figures(launches, launch_ms)
 
-    # per-launch durations (HIP events on the launch stream), for the per-N figures and roofline
-    per = [[0.0 for _ in mats]]
-    for _ in range(args.steps):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in mats]
-        step(ev)
-        torch.cuda.synchronize()
-        for i, (a, b) in enumerate(ev):
-            per[0][i] += a.elapsed_time(b) / args.steps
-    launch_ms = per[0]
-
-    total_vectors = sum(spec.rows for spec, *_ in mats)
-    value = total_vectors / (ms_per_step / 1e3)
-    by_n = {}
-    for (spec, *_), ms in zip(mats, launch_ms):
-        d = by_n.setdefault(spec.n, {"vectors": 0, "ms": 0.0, "flops": 0.0, "bytes": 0})
-        d["vectors"] += spec.rows
-        d["ms"] += ms
-        d["flops"] += spec.rows * counted_flops_per_vector(spec.n, wl.iters)
-        d["bytes"] += spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4)
-    per_n = {}
-    for n, d in sorted(by_n.items()):
-        s = d["ms"] / 1e3
-        per_n[str(n)] = {
-            "vectors_per_s": d["vectors"] / s,
-            "counted_tflops": d["flops"] / s / 1e12,
-            "valu_frac": d["flops"] / s / 1e12 / PEAK_FP32_TFLOPS,
-            "hbm_gbps": d["bytes"] / s / 1e9,
-            "ms_per_step": d["ms"],
-        }
-    # dominant kernel: the N = 4096 pair kernel (if present), averaged over its launches
+    # dominant kernel: the N = 4096 launches (if present), averaged over them
     dom_n = 4096 if 4096 in by_n else max(by_n, key=lambda n: by_n[n]["ms"])
-    dom = [(spec, ms) for (spec, *_), ms in zip(mats, launch_ms) if spec.n == dom_n]
-    dom_flops = sum(spec.rows * counted_flops_per_vector(spec.n, wl.iters) for spec, _ in dom)
+    dom = [(l, ms) for l, ms in zip(launches, launch_ms) if l.n == dom_n]
     dom_s = sum(ms for _, ms in dom) / 1e3
-    achieved = dom_flops / dom_s / 1e12
-    dom_bytes = sum(spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4)
-                    for spec, _ in dom) / len(dom)
-    traffic = measured_traffic([(spec.n, (spec.rows + 1) // 2) for spec, _ in dom])
+    dom_flops = sum(l.flops for l, _ in dom)
+    dom_bytes = sum(l.nbytes for l, _ in dom)
+    if args.op == "quantize":
+        achieved = dom_flops / dom_s / 1e12
+        roofline = {
+            "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_TFLOPS,
+            "traffic": measured_traffic("quantize", args.workload, "pair_greedy_kernel[quantize]",
+                                        [(l.n, (l.rows + 1) // 2) for l, _ in dom]),
+            "kernel": f"pair_greedy_kernel[quantize] N={dom_n}", "launches": len(dom),
+            "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
+            "algorithmic_bytes_per_launch": dom_bytes / len(dom),
+        }
+        metric, unit = METRIC, "vectors/s"
+        workload = (f"{args.workload}: " + ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices)
+                    + f" x {wl.layers} layer(s), {wl.matrices[0].dtype} storage, k={wl.iters} blocks, "
+                    f"lloyd={args.lloyd}, one row = one vector")
+    else:
+        achieved = dom_bytes / dom_s / 1e9
+        roofline = {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBPS,
+            "traffic": measured_traffic(args.op, args.workload, "pair_pmap_kernel",
+                                        [(l.n, min((l.rows + 1) // 2, PMAP_GRID)) for l, _ in dom]),
+            "kernel": f"pair_pmap_kernel N={dom_n}", "launches": len(dom),
+            "valu_tflops": dom_flops / dom_s / 1e12,
+            "algorithmic_bytes_per_launch": dom_bytes / len(dom),
+        }
+        if args.op == "apply_p":
+            metric, unit = METRIC_APPLY_P, "rows/s"
+            workload = (f"apply_p: {args.act_rows} Gaussian fp32 rows at each width "
+                        + ", ".join(str(n) for n in sorted(by_n)) + f" ({args.workload} input widths)")
+        else:
+            metric, unit = METRIC_RECON, "rows/s"
+            workload = (f"reconstruct: {args.workload} " + ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices)
+                        + f" x {wl.layers} layer(s) from their 2+2-bit codes (k={wl.iters}), fp32 output")
     result = {
-        "metric": METRIC,
-        "value": value,
-        "unit": "vectors/s",
+        "metric": metric,
+        "value": total_vectors / (ms_per_step / 1e3),
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -224,31 +334,17 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {
-            "workload": f"{args.workload}: " + ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices)
-                        + f" x {wl.layers} layer(s), {wl.matrices[0].dtype} storage, k={wl.iters} blocks, "
-                        f"lloyd={args.lloyd}, one row = one vector",
-            "vectors_per_step": total_vectors,
-            "iters": wl.iters,
-        },
+        "config": {"workload": workload, "vectors_per_step": total_vectors, "iters": wl.iters},
         "per_n": per_n,
-        "roofline": {
-            "bound": "alu",
-            "achieved": achieved,
-            "peak": PEAK_FP32_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_TFLOPS,
-            "traffic": traffic,
-            "kernel": f"pair_greedy_kernel N={dom_n}",
-            "launches": len(dom),
-            "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
-            "algorithmic_bytes_per_launch": dom_bytes,
-        },
+        "roofline": roofline,
         "source_digest": source_digest(),
     }
     if not args.no_cpu_baseline:
-        log(f"cpu baseline: oracle on {args.cpu_rows} rows")
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows)
+        if args.op == "quantize":
+            log(f"cpu baseline: oracle on {args.cpu_rows} rows")
+            result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows)
+        elif args.op == "apply_p":
+            result["cpu_baseline"] = cpu_baseline_apply_p(dom_n, 4 * args.cpu_rows)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -907,14 +907,16 @@ __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(__half v) { return __half2float(v); }
 
 // Load rows a (and b if >= 0) into the greedy register layout, in even/odd order.
+// `tid` is the thread index (a laundered copy in loops whose other values are invariant, so
+// that the element offsets are recomputed rather than kept live across the loop).
 template <class C, class IT>
 __device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restrict__ w, int64_t ldw, int64_t ra,
-                                            int64_t rb) {
+                                            int64_t rb, int tid = static_cast<int>(threadIdx.x)) {
   const IT* __restrict__ pa = w + ra * ldw;
   const IT* __restrict__ pb = w + (rb >= 0 ? rb : ra) * ldw;
 #pragma unroll
   for (int i = 0; i < C::B0; ++i) {
-    const int j = threadIdx.x + C::T * i;
+    const int j = tid + C::T * i;
 #pragma unroll
     for (int r = 0; r < C::R0; ++r) {
       float2 v = make_float2(0.f, 0.f);
@@ -934,9 +936,9 @@ __device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restr
 
 template <class C>
 __device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
-                                          int64_t rb) {
-  if (dtype == 1) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb);
-  else load_pair_t<C>(z, static_cast<const float*>(w), ldw, ra, rb);
+                                          int64_t rb, int tid = static_cast<int>(threadIdx.x)) {
+  if (dtype == 1) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, tid);
+  else load_pair_t<C>(z, static_cast<const float*>(w), ldw, ra, rb, tid);
 }
 
 // z <- w * scale - z for the pair (rows reloaded in the register layout); zero for a bad row.
@@ -953,10 +955,10 @@ __device__ __forceinline__ void sub_from_rows(float2 (&z)[C::E], const void* w, 
 }
 
 template <class C, class F>
-__device__ __forceinline__ void for_each_elem(F&& f) {
+__device__ __forceinline__ void for_each_elem(F&& f, int tid = static_cast<int>(threadIdx.x)) {
 #pragma unroll
   for (int i = 0; i < C::B0; ++i) {
-    const int j = threadIdx.x + C::T * i;
+    const int j = tid + C::T * i;
     if (j < C::NB0) {
 #pragma unroll
       for (int r = 0; r < C::R0; ++r) f(i * C::R0 + r, orig_index<C::N>(j + r * C::NB0));
@@ -1004,6 +1006,13 @@ __device__ __forceinline__ void sort4(float (&q)[4]) {
   cx(q[0], q[2]);
   cx(q[1], q[3]);
   cx(q[1], q[2]);
+}
+
+// q[c] for a 2-bit code c held in a register (selects, no indexed access)
+__device__ __forceinline__ float pick4(const float (&q)[4], uint32_t c) {
+  const float lo = (c & 1) ? q[1] : q[0];
+  const float hi = (c & 1) ? q[3] : q[2];
+  return (c & 2) ? hi : lo;
 }
 
 __device__ __forceinline__ int code_of(float x, const float (&mids)[3]) {
@@ -1295,56 +1304,125 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
 
 // ------------------------------------------------------------------ P-only kernel
 // MODE_APPLY_P: y = P x.  MODE_RECON: w_hat = u_q + P v_q from codes and centres.
+// Persistent over pairs: the grid is capped and each workgroup walks items
+// blockIdx.x, blockIdx.x + gridDim.x, ... so the operator constants are loaded once per
+// workgroup, not once per pair (one application of P is cheap next to them).  The
+// reconstruction moves its rows between HBM and the FFT's register layout through the LDS
+// buffer, in row order, so codes are read one byte per four elements and w_hat is written in
+// contiguous 16-byte vectors; y = P x loads and stores in the register layout directly
+// (measured faster for it than staging).
 template <class C>
-__global__ __launch_bounds__(C::T) void pair_pmap_kernel(KArgs a, int64_t item0) {
+__global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_pmap_kernel(
+    KArgs a, int64_t item0, int64_t nitems) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
   __shared__ float red[2 * C::NW * 32];
-  const int64_t item = item0 + blockIdx.x;
-  const int64_t ra = 2 * item;
-  const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
+  constexpr int N = C::N;
+  constexpr int NBY = (N + 3) / 4;
+  static_assert(N % 4 == 0, "row staging in 16-byte vectors");
   int slot = 0;
-  constexpr int NBY = (C::N + 3) / 4;
-  float2 z[C::E];
-  if (a.mode == MODE_APPLY_P) {
-    load_pair<C>(z, a.w, /*fp32*/ 0, a.ldw, ra, rb);
-  } else {
-    const uint8_t* cv = a.in_codes_v;
-    const float* ce = a.in_centers;
+  constexpr bool RES = resident_ok<C>();
+  ResRegs<C> rr;
+  if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
+  const float qnan = __int_as_float(0x7fc00000);
+  float* lf = reinterpret_cast<float*>(lds);  // staging: row a at [0, N), row b at [N, 2N)
+  float4* lf4 = reinterpret_cast<float4*>(lds);
+  const bool recon = a.mode == MODE_RECON;
+  const bool vout = (reinterpret_cast<uintptr_t>(a.y) % 16 == 0) && (a.ldy % 4 == 0);
+  for (int64_t it = blockIdx.x; it < nitems; it += gridDim.x) {
+    const int64_t ra = 2 * (item0 + it);
+    const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
+    const int tid = opaque(static_cast<int>(threadIdx.x));
+    float2 z[C::E];
 #pragma unroll
     for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
-    for_each_elem<C>([&](int e, int i) {
-      const int sh = 2 * (i & 3);
-      const int ca = (cv[ra * NBY + (i >> 2)] >> sh) & 3;
-      z[e].x = ce[ra * 8 + 4 + ca];
-      if (rb >= 0) {
-        const int cb2 = (cv[rb * NBY + (i >> 2)] >> sh) & 3;
-        z[e].y = ce[rb * 8 + 4 + cb2];
+    // 1. y = P x reads its rows straight into the register layout; the reconstruction decodes
+    // the v codes in row order into LDS (row b zero when absent)
+    if (!recon) {
+      load_pair<C>(z, a.w, /*fp32*/ 0, a.ldw, ra, rb, tid);
+    } else {
+      const float* cea = a.in_centers + ra * 8 + 4;
+      const float* ceb = a.in_centers + (rb >= 0 ? rb : ra) * 8 + 4;
+      const float qa[4] = {cea[0], cea[1], cea[2], cea[3]};
+      const float qb[4] = {ceb[0], ceb[1], ceb[2], ceb[3]};
+      const uint8_t* cva = a.in_codes_v + ra * NBY;
+      const uint8_t* cvb = a.in_codes_v + (rb >= 0 ? rb : ra) * NBY;
+      for (int q = tid; q < NBY; q += C::T) {
+        const uint32_t ba = cva[q], bb = cvb[q];
+        float4 va, vb;
+        va.x = pick4(qa, ba & 3);
+        va.y = pick4(qa, (ba >> 2) & 3);
+        va.z = pick4(qa, (ba >> 4) & 3);
+        va.w = pick4(qa, (ba >> 6) & 3);
+        vb.x = pick4(qb, bb & 3);
+        vb.y = pick4(qb, (bb >> 2) & 3);
+        vb.z = pick4(qb, (bb >> 4) & 3);
+        vb.w = pick4(qb, (bb >> 6) & 3);
+        lf4[q] = va;
+        lf4[N / 4 + q] = rb >= 0 ? vb : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-    });
-  }
-  float2 scale, unscale;
-  bool bad_a, bad_b;
-  normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
-  if constexpr (resident_ok<C>()) {
-    ResRegs<C> rr;
-    resident_load<C>(rr, lds, a.tw, a.mid4);
-    apply_P_res<C>(z, lds, rr);
-  } else {
-    apply_P<C>(z, lds, a.tw, a.mid4);
-  }
-  const float qnan = __int_as_float(0x7fc00000);
-  const uint8_t* cu = static_cast<const uint8_t*>(a.w);
-  for_each_elem<C>([&](int e, int i) {
-    float va = bad_a ? qnan : z[e].x * unscale.x;
-    float vb = bad_b ? qnan : z[e].y * unscale.y;
-    if (a.mode == MODE_RECON) {
-      const int sh = 2 * (i & 3);
-      va += a.in_centers[ra * 8 + ((cu[ra * NBY + (i >> 2)] >> sh) & 3)];
-      if (rb >= 0) vb += a.in_centers[rb * 8 + ((cu[rb * NBY + (i >> 2)] >> sh) & 3)];
     }
-    a.y[ra * a.ldy + i] = va;
-    if (rb >= 0) a.y[rb * a.ldy + i] = vb;
-  });
+    if (recon) {
+      __syncthreads();
+      for_each_elem<C>([&](int e, int i) { z[e] = make_float2(lf[i], lf[N + i]); }, tid);
+      __syncthreads();  // the staged v_q rows are read before the first pass overwrites the buffer
+    }
+    float2 scale, unscale;
+    bool bad_a, bad_b;
+    normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
+    if constexpr (RES) apply_P_res<C>(z, lds, rr);
+    else apply_P<C>(z, lds, a.tw, a.mid4);
+    if (!recon) {
+      for_each_elem<C>([&](int e, int i) {
+        a.y[ra * a.ldy + i] = bad_a ? qnan : z[e].x * unscale.x;
+        if (rb >= 0) a.y[rb * a.ldy + i] = bad_b ? qnan : z[e].y * unscale.y;
+      }, tid);
+      __syncthreads();  // the last pass read the buffer the next item's first pass writes
+      continue;
+    }
+    __syncthreads();  // the last pass read the buffer the outputs are staged in
+    for_each_elem<C>([&](int e, int i) {
+      lf[i] = bad_a ? qnan : z[e].x * unscale.x;
+      lf[N + i] = bad_b ? qnan : z[e].y * unscale.y;
+    }, tid);
+    __syncthreads();
+    // 2. reconstruction: w_hat = P v_q + u_q in row order, 16-byte stores
+    const uint8_t* cua = static_cast<const uint8_t*>(a.w) + ra * NBY;
+    const uint8_t* cub = static_cast<const uint8_t*>(a.w) + (rb >= 0 ? rb : ra) * NBY;
+    const float* cea = a.in_centers + ra * 8;
+    const float* ceb = a.in_centers + (rb >= 0 ? rb : ra) * 8;
+    const float ua[4] = {cea[0], cea[1], cea[2], cea[3]};
+    const float ub[4] = {ceb[0], ceb[1], ceb[2], ceb[3]};
+    float* ya = a.y + ra * a.ldy;
+    float* yb = a.y + (rb >= 0 ? rb : ra) * a.ldy;
+    for (int q = tid; q < N / 4; q += C::T) {
+      float4 oa = lf4[q], ob = lf4[N / 4 + q];
+      const uint32_t ba = cua[q], bb = cub[q];
+      oa.x += pick4(ua, ba & 3);
+      oa.y += pick4(ua, (ba >> 2) & 3);
+      oa.z += pick4(ua, (ba >> 4) & 3);
+      oa.w += pick4(ua, (ba >> 6) & 3);
+      ob.x += pick4(ub, bb & 3);
+      ob.y += pick4(ub, (bb >> 2) & 3);
+      ob.z += pick4(ub, (bb >> 4) & 3);
+      ob.w += pick4(ub, (bb >> 6) & 3);
+      if (vout) {
+        reinterpret_cast<float4*>(ya)[q] = oa;
+        if (rb >= 0) reinterpret_cast<float4*>(yb)[q] = ob;
+      } else {
+        ya[4 * q] = oa.x;
+        ya[4 * q + 1] = oa.y;
+        ya[4 * q + 2] = oa.z;
+        ya[4 * q + 3] = oa.w;
+        if (rb >= 0) {
+          yb[4 * q] = ob.x;
+          yb[4 * q + 1] = ob.y;
+          yb[4 * q + 2] = ob.z;
+          yb[4 * q + 3] = ob.w;
+        }
+      }
+    }
+    __syncthreads();  // staged outputs read before the next item stages its inputs
+  }
 }
 
 // ------------------------------------------------------------------ dispatch
@@ -1363,7 +1441,9 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
       hipLaunchKernelGGL((pair_greedy_kernel<C, false, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
                          i0);
     } else {
-      hipLaunchKernelGGL(pair_pmap_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
+      constexpr int64_t kPmapGrid = 2048;  // resident workgroups of the whole chip, a few times over
+      const int64_t pg = g < kPmapGrid ? g : kPmapGrid;
+      hipLaunchKernelGGL(pair_pmap_kernel<C>, dim3(static_cast<unsigned>(pg)), dim3(C::T), 0, s, a, i0, g);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -9,8 +9,8 @@ number of dispatches and the average duration.  The four counter databases (one
 `--pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` run of the same program, and the same two of a
 plain 256 MiB device copy) give HBM bytes per dispatch: the raw KiB figure times the factor
 that makes the copy's counter read its known size.  The last line of the output,
-`TRAFFIC_JSON {...}`, carries those bytes per (vector length, workgroups) together with the
-digest of the kernel sources they were taken on.
+`TRAFFIC_JSON {...}`, carries those bytes per (kernel, vector length, workgroups) together with
+the digest of the kernel sources they were taken on.
 """
 from __future__ import annotations
 
@@ -107,8 +107,8 @@ def main() -> int:
             k, n, wg, wx = key
             b = fetch[key] * 1024 * f_fac + write[key] * 1024 * w_fac
             out.append(f"  {k:28s} {n:6d} {wg:6d} {fetch[key]:11.1f} {write[key]:11.1f} {b:12.4g}")
-            if k.startswith("pair_greedy_kernel[quantize"):
-                traffic["bytes"][f"{n}/{wg}"] = b
+            if k.startswith("pair_"):
+                traffic["bytes"][f"{k}|{n}/{wg}"] = b
     print("\n".join(out))
     if traffic is not None:
         print("TRAFFIC_JSON " + json.dumps(traffic, sort_keys=True))

@@ -69,6 +69,50 @@ def test_apply_p_matches_oracle(n):
     assert np.abs(y2.cpu().numpy() - x).max() / scale <= 1e-5
 
 
+@pytest.mark.parametrize("n", [4096, 11008])
+def test_apply_p_bench_batch(n):
+    """y = P x on the benchmark's activation batch (16384 fp32 rows per width, one launch as
+    bench.py --op apply_p times it): sampled rows against the oracle."""
+    g = torch.Generator(device="cuda").manual_seed(n)
+    x = torch.randn((16384, n), dtype=torch.float32, device="cuda", generator=g)
+    y = torch.empty_like(x)
+    plan = K.kashin_plan(n, 0, 1)
+    K.kashin_apply_p(plan, x, y)
+    torch.cuda.synchronize()
+    rows = [0, 1, 2, 4097, 8191, 12345, 16382, 16383]
+    xs = x[rows].cpu().numpy().astype(np.float64)
+    yref = ref.apply_p(xs, ref.sign_mask(n, 0))
+    err = np.abs(y[rows].cpu().numpy() - yref).max() / max(np.abs(xs).max(), np.abs(yref).max())
+    _say(f"apply_p batch N={n}: max err / scale = {err:.2e}")
+    assert err <= 5e-6
+
+
+def test_reconstruct_layer_sampled_rows():
+    """w_hat = u_q + P v_q for the llama7b layer's down_proj and q_proj (full matrices, one
+    launch each as bench.py --op reconstruct times them), sampled rows against the oracle's
+    reconstruction from the same codes and centres."""
+    wl = synth.WORKLOADS["llama7b"]
+    names = [s.name for s in wl.matrices]
+    for name in ("q_proj", "down_proj"):
+        idx = names.index(name)
+        spec = wl.matrices[idx]
+        seed = synth.sign_seed(wl, 0, idx)
+        plan = K.kashin_plan(spec.n, seed, wl.iters)
+        wd = pu.to_dev(synth.make_matrix(wl, 0, idx)).to(torch.float16)
+        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+        wh = torch.empty((spec.rows, spec.n), dtype=torch.float32, device="cuda")
+        K.kashin_reconstruct(plan, cu, cv, ce, wh)
+        torch.cuda.synchronize()
+        rows = [0, 1, spec.rows // 2, spec.rows - 1]
+        cu_s = pu.unpack(cu.cpu().numpy()[rows], spec.n)
+        cv_s = pu.unpack(cv.cpu().numpy()[rows], spec.n)
+        ce_s = ce.cpu().numpy()[rows].astype(np.float64)
+        wref = ref.reconstruct(cu_s, cv_s, ce_s, ref.sign_mask(spec.n, seed))
+        err = np.abs(wh.cpu().numpy()[rows] - wref).max() / np.abs(wref).max()
+        _say(f"reconstruct {name} N={spec.n}: max err / max|w_hat| = {err:.2e}")
+        assert err <= 1e-5
+
+
 # ----------------------------------------------------------------------------- Alg. 2 on small batches
 CASES = [(64, 3, "gauss"), (96, 20, "gauss"), (172, 20, "t4"), (256, 1, "gauss"), (512, 20, "gauss"),
          (768, 30, "outlier"), (1024, 8, "t4"), (2048, 20, "gauss"), (3072, 30, "outlier"), (4096, 30, "t4"),
@@ -236,6 +280,31 @@ def test_empty_single_and_strided_rows():
     assert rec.max() <= 1e-5 * np.abs(w64).max()
     # the unpaired last row of the 3-row call equals the 1-row call bit for bit
     np.testing.assert_array_equal(u.cpu().numpy()[2], u1.cpu().numpy()[0])
+
+
+def test_unaligned_and_strided_p_map_io():
+    """apply_p from/to buffers that are not 16-byte aligned and reconstruct into strided rows
+    take the scalar staging path; results equal the aligned, contiguous calls bit for bit."""
+    n, m = 512, 5
+    plan = K.kashin_plan(n, 3, 6)
+    rng = np.random.default_rng(8)
+    x = pu.to_dev(_rows(rng, m, n))
+    y = torch.empty_like(x)
+    K.kashin_apply_p(plan, x, y)
+    xbuf = torch.zeros(m * n + 1, dtype=torch.float32, device="cuda")
+    ybuf = torch.zeros(m * n + 1, dtype=torch.float32, device="cuda")
+    xbuf[1:].copy_(x.reshape(-1))
+    xo, yo = xbuf[1:].view(m, n), ybuf[1:].view(m, n)
+    K.kashin_apply_p(plan, xo, yo)
+    cu, cv, ce = K.quantize_alloc(plan, x, 0)
+    wh = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    K.kashin_reconstruct(plan, cu, cv, ce, wh)
+    wide = torch.zeros((m, n + 3), dtype=torch.float32, device="cuda")
+    K.kashin_reconstruct(plan, cu, cv, ce, wide[:, :n])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(yo.cpu().numpy(), y.cpu().numpy())
+    np.testing.assert_array_equal(wide[:, :n].cpu().numpy(), wh.cpu().numpy())
+    assert (wide[:, n:] == 0).all()
 
 
 def test_nonfinite_row_is_isolated():
