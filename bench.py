@@ -10,6 +10,10 @@
   input width N of the workload (the inference-side product of App. C).
 --op reconstruct: one step = w_hat = u_q + P v_q (kashin_reconstruct) from the codes and centres
   of every matrix of the workload (quantized once, untimed).
+--op rotate: one step = the incoherence pre-rotation R w (kashin_rotate) of every matrix of the
+  workload, fp16 rows in, fp32 rows out.
+--op quantize_h: one step = the "+H" pipeline, R w followed by kashin_quantize of the rotated
+  rows, for every matrix of the workload.
 """
 from __future__ import annotations
 
@@ -29,6 +33,9 @@ if ROOT not in sys.path:
 METRIC = "weight vectors decomposed/s (N=4096, fixed iters); % of HBM / FP32 VALU roofline"
 METRIC_APPLY_P = "activation rows transformed/s (y = P x, fp32); % of HBM roofline"
 METRIC_RECON = "weight rows reconstructed/s (w_hat = u_q + P v_q from 2+2-bit codes, fp32 out); % of HBM roofline"
+METRIC_ROTATE = "weight rows rotated/s (R w, fp16 in, fp32 out); % of HBM roofline"
+METRIC_QUANT_H = "weight vectors rotated + decomposed + quantised/s (+H pipeline, N=4096, fixed iters)"
+ROT_SEED = 1234  # seed of the rotation's sign vector
 PEAK_FP32_TFLOPS = 157.3   # MI355X published FP32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
 PEAK_HBM_GBPS = 8000.0     # MI355X published HBM3E bandwidth
 PMAP_GRID = 2048           # workgroups of a P-only launch (the library's cap; each walks several pairs)
@@ -61,6 +68,7 @@ class Launch:
     flops: float          # counted flops of the launch
     nbytes: float         # algorithmic HBM bytes of the launch
     run: Callable         # run(stream)
+    kind: str = "quantize"  # which kernel the launch runs: quantize, pmap or rotate
 
 
 def measured_traffic(op: str, workload: str, kernel: str, launches) -> float | None:
@@ -199,7 +207,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
-    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct"), default="quantize")
+    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h"),
+                    default="quantize")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
@@ -235,7 +244,7 @@ def main() -> int:
     launches: list[Launch] = []
     keep = []  # device buffers and plans referenced by the launches
 
-    if args.op in ("quantize", "reconstruct"):
+    if args.op in ("quantize", "reconstruct", "rotate", "quantize_h"):
         for layer in range(wl.layers):
             for idx, spec in enumerate(wl.matrices):
                 log(f"generating {args.workload} layer {layer} {spec.name} {spec.rows}x{spec.n}")
@@ -248,7 +257,23 @@ def main() -> int:
                 cu = torch.empty((spec.rows, nb), dtype=torch.uint8, device=dev)
                 cv = torch.empty_like(cu)
                 ce = torch.empty((spec.rows, 2, 4), dtype=torch.float32, device=dev)
-                if args.op == "quantize":
+                if args.op in ("rotate", "quantize_h"):
+                    wr = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
+                    keep.append((plan, wd, wr, cu, cv, ce))
+                    p2 = spec.n & -spec.n
+                    launches.append(Launch(
+                        spec.n, spec.rows, spec.rows * spec.n * (math.log2(p2) + 2 * (spec.n // p2)),
+                        spec.rows * spec.n * (2 + 4),
+                        lambda s, a=(spec.n, wd, wr): K.kashin_rotate(a[0], ROT_SEED, a[1], a[2], stream=s),
+                        kind="rotate"))
+                    if args.op == "quantize_h":
+                        launches[-1].rows = 0  # counted once, on its quantize launch
+                        launches.append(Launch(
+                            spec.n, spec.rows, spec.rows * counted_flops_per_vector(spec.n, wl.iters),
+                            spec.rows * hbm_bytes_per_vector(spec.n, 4),
+                            lambda s, a=(plan, wr, cu, cv, ce): K.kashin_quantize(a[0], a[1], args.lloyd, a[2], a[3],
+                                                                                  a[4], s)))
+                elif args.op == "quantize":
                     keep.append((plan, wd, cu, cv, ce))
                     launches.append(Launch(
                         spec.n, spec.rows, spec.rows * counted_flops_per_vector(spec.n, wl.iters),
@@ -264,7 +289,8 @@ def main() -> int:
                     launches.append(Launch(
                         spec.n, spec.rows, spec.rows * 2 * transform_flops(spec.n),
                         spec.rows * (2 * nb + 32 + 4 * spec.n),
-                        lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s)))
+                        lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s),
+                        kind="pmap"))
     else:
         g = torch.Generator(device=dev).manual_seed(0)
         for n in sorted({spec.n for spec in wl.matrices}):
@@ -274,42 +300,50 @@ def main() -> int:
             plan = K.kashin_plan(n, 0, 1)
             keep.append((plan, x, y))
             launches.append(Launch(n, args.act_rows, args.act_rows * 2 * transform_flops(n), args.act_rows * 8 * n,
-                                   lambda s, a=(plan, x, y): K.kashin_apply_p(a[0], a[1], a[2], s)))
+                                   lambda s, a=(plan, x, y): K.kashin_apply_p(a[0], a[1], a[2], s), kind="pmap"))
     torch.cuda.synchronize()
 
     ms_per_step, launch_ms = time_launches(launches, args.steps, args.warmup, stream)
     total_vectors = sum(l.rows for l in launches)
     by_n, per_n = per_n_figures(launches, launch_ms)
 
-    # dominant kernel: the N = 4096 launches (if present), averaged over them
+    # dominant kernel: the N = 4096 launches (if present) of the op's main kernel, averaged over them
+    main_kind = {"quantize": "quantize", "quantize_h": "quantize", "rotate": "rotate"}.get(args.op, "pmap")
     dom_n = 4096 if 4096 in by_n else max(by_n, key=lambda n: by_n[n]["ms"])
-    dom = [(l, ms) for l, ms in zip(launches, launch_ms) if l.n == dom_n]
+    dom = [(l, ms) for l, ms in zip(launches, launch_ms) if l.n == dom_n and l.kind == main_kind]
     dom_s = sum(ms for _, ms in dom) / 1e3
     dom_flops = sum(l.flops for l, _ in dom)
     dom_bytes = sum(l.nbytes for l, _ in dom)
-    if args.op == "quantize":
+    layer = ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices) + f" x {wl.layers} layer(s)"
+    if main_kind == "quantize":
         achieved = dom_flops / dom_s / 1e12
         roofline = {
             "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_TFLOPS,
-            "traffic": measured_traffic("quantize", args.workload, "pair_greedy_kernel[quantize]",
+            "traffic": measured_traffic(args.op, args.workload, "pair_greedy_kernel[quantize]",
                                         [(l.n, (l.rows + 1) // 2) for l, _ in dom]),
             "kernel": f"pair_greedy_kernel[quantize] N={dom_n}", "launches": len(dom),
             "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
             "algorithmic_bytes_per_launch": dom_bytes / len(dom),
         }
-        metric, unit = METRIC, "vectors/s"
-        workload = (f"{args.workload}: " + ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices)
-                    + f" x {wl.layers} layer(s), {wl.matrices[0].dtype} storage, k={wl.iters} blocks, "
-                    f"lloyd={args.lloyd}, one row = one vector")
+        if args.op == "quantize":
+            metric, unit = METRIC, "vectors/s"
+            workload = (f"{args.workload}: {layer}, {wl.matrices[0].dtype} storage, k={wl.iters} blocks, "
+                        f"lloyd={args.lloyd}, one row = one vector")
+        else:
+            metric, unit = METRIC_QUANT_H, "vectors/s"
+            workload = (f"{args.workload} +H: {layer}, {wl.matrices[0].dtype} rows rotated (R w, seed {ROT_SEED}) "
+                        f"to fp32, then quantised, k={wl.iters} blocks, lloyd={args.lloyd}")
     else:
         achieved = dom_bytes / dom_s / 1e9
+        kname = f"rotate_kernel[b={dom_n // (dom_n & -dom_n)}]" if main_kind == "rotate" else "pair_pmap_kernel"
+        grid = (lambda l: l.rows) if main_kind == "rotate" else (lambda l: min((l.rows + 1) // 2, PMAP_GRID))
+        keyn = (lambda l: 0) if main_kind == "rotate" else (lambda l: l.n)  # the rotation kernel takes n at run time
         roofline = {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBPS,
-            "traffic": measured_traffic(args.op, args.workload, "pair_pmap_kernel",
-                                        [(l.n, min((l.rows + 1) // 2, PMAP_GRID)) for l, _ in dom]),
-            "kernel": f"pair_pmap_kernel N={dom_n}", "launches": len(dom),
+            "traffic": measured_traffic(args.op, args.workload, kname, [(keyn(l), grid(l)) for l, _ in dom]),
+            "kernel": f"{kname} N={dom_n}", "launches": len(dom),
             "valu_tflops": dom_flops / dom_s / 1e12,
             "algorithmic_bytes_per_launch": dom_bytes / len(dom),
         }
@@ -317,10 +351,13 @@ def main() -> int:
             metric, unit = METRIC_APPLY_P, "rows/s"
             workload = (f"apply_p: {args.act_rows} Gaussian fp32 rows at each width "
                         + ", ".join(str(n) for n in sorted(by_n)) + f" ({args.workload} input widths)")
+        elif args.op == "rotate":
+            metric, unit = METRIC_ROTATE, "rows/s"
+            workload = f"rotate: {args.workload} {layer}, fp16 rows in, fp32 rows out (seed {ROT_SEED})"
         else:
             metric, unit = METRIC_RECON, "rows/s"
-            workload = (f"reconstruct: {args.workload} " + ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices)
-                        + f" x {wl.layers} layer(s) from their 2+2-bit codes (k={wl.iters}), fp32 output")
+            workload = (f"reconstruct: {args.workload} {layer} from their 2+2-bit codes (k={wl.iters}), "
+                        f"fp32 output")
     result = {
         "metric": metric,
         "value": total_vectors / (ms_per_step / 1e3),

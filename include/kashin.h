@@ -110,6 +110,23 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
  * x and y may not alias. */
 int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream);
 
+/* Incoherence pre-rotation of rows, the "+H" preprocessing of Sec. 5 (the paper names a
+ * QuIP-style randomised Hadamard transform, with a Kronecker variant, applied to the weights
+ * before the decomposition; it gives no construction, so this one is a reading):
+ *   R = (H_{2^a} / sqrt(2^a) kron C_b) diag(s),   n = 2^a b, b odd,
+ * H the Sylvester Hadamard matrix, C_b the orthonormal DCT-II of length b (C_1 = [1]), element
+ * index i b + j for segment i and position j, s_i = -1 when the top bit of the i-th splitmix64
+ * output of `seed` is set (the generator of kashin_signs).  R is orthogonal.
+ * y = R x (inverse = 0) or y = R^T x (inverse = 1) for m rows.
+ *   n       odd part b in {1, 3, 43}, n <= 16384 (else KASHIN_E_UNSUPPORTED_N)
+ *   x       m rows, dtype KASHIN_F32 or KASHIN_F16, leading dimension ldx >= n (device)
+ *   y       m fp32 rows, leading dimension ldy >= n (device); y == x is allowed (in place) for
+ *           fp32 with ldy == ldx, any other overlap is KASHIN_E_INVALID
+ * Plan-free: runs on the current device.  Quantising R w and reconstructing R^T w_hat
+ * composes the rotation with the rest of the path. */
+int kashin_rotate(int32_t n, uint64_t seed, int32_t inverse, const void* x, int32_t dtype, int64_t m,
+                  int64_t ldx, float* y, int64_t ldy, void* stream);
+
 /* Test hook: replay record of Alg. 2 for selected rows.  For each of the `nrows` row
  * indices in `rows` (device int64, each in [0, m)), the row is decomposed exactly as
  * kashin_decompose does (paired with the same neighbour) and the kernel writes

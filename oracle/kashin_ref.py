@@ -32,6 +32,13 @@ of Language Models"):
 * ``optimal4_sse`` -- exact optimum of 1-D 4-level clustering (brute force over
   contiguous partitions of the sorted values, or an O(4 n^2) dynamic program),
   used to pin the clustering.
+* ``hadamard_matrix`` / ``rotation_matrix`` / ``rotate`` -- the incoherence
+  pre-rotation applied to weight rows before the decomposition (the "+H"
+  preprocessing of Sec. 5; the paper only names a QuIP-style randomised
+  Hadamard transform, with a Kronecker variant).  Reading: for n = 2^a b with
+  b odd, R = (H_{2^a} / sqrt(2^a) kron C_b) diag(s), H the Sylvester Hadamard
+  matrix, C_b the orthonormal DCT-II of length b (C_1 = [1]), s = sign_mask(n,
+  seed).
 
 Every function is pinned by ``tests/test_oracle_*.py`` against facts the paper
 and the mathematics fix (library DCT, orthonormality, involution, the exact
@@ -65,6 +72,9 @@ __all__ = [
     "quantize",
     "optimal4_sse",
     "sse4",
+    "hadamard_matrix",
+    "rotation_matrix",
+    "rotate",
 ]
 
 _MASK64 = (1 << 64) - 1
@@ -422,3 +432,44 @@ def optimal4_sse(x):
             nd[j] = min(dp[i] + cost(i, j) for i in range(j + 1))
         dp = nd
     return float(dp[n])
+
+
+# ---------------------------------------------------------------------------
+# Incoherence pre-rotation (Sec. 5: the "+H" variant rotates the weights with a
+# randomised Hadamard transform before the decomposition; the Kronecker form covers
+# widths that are not powers of two).
+# ---------------------------------------------------------------------------
+def hadamard_matrix(m: int) -> np.ndarray:
+    """Sylvester's Hadamard matrix of order m = 2^a (entries +-1): H_1 = [1],
+    H_2k = [[H_k, H_k], [H_k, -H_k]]."""
+    if m < 1 or m & (m - 1):
+        raise ValueError("order must be a power of two")
+    h = np.ones((1, 1))
+    while h.shape[0] < m:
+        h = np.block([[h, h], [h, -h]])
+    return h
+
+
+def _split_pow2(n: int) -> tuple[int, int]:
+    """n = 2^a * b with b odd -> (2^a, b)."""
+    p2 = n & -n
+    return p2, n // p2
+
+
+@functools.lru_cache(maxsize=2)
+def rotation_matrix(n: int, seed: int) -> np.ndarray:
+    """R = (H_{2^a} / sqrt(2^a) kron C_b) diag(s) for n = 2^a b, b odd (orthogonal)."""
+    p2, b = _split_pow2(n)
+    hb = hadamard_matrix(p2) / np.sqrt(p2)
+    cb = dct2_matrix(b) if b > 1 else np.ones((1, 1))
+    r = np.kron(hb, cb) * sign_mask(n, seed).astype(np.float64)[None, :]
+    r.setflags(write=False)
+    return r
+
+
+def rotate(x: np.ndarray, seed: int, inverse: bool = False) -> np.ndarray:
+    """Row-wise R x (or R^T x with inverse) for a batch of rows x (B, n)."""
+    x = np.asarray(x, dtype=np.float64)
+    r = rotation_matrix(x.shape[1], seed)
+    return x @ r if inverse else x @ r.T
+

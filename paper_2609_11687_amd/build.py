@@ -43,7 +43,8 @@ def _hipcc() -> str:
 
 
 def sources() -> list[str]:
-    srcs = [os.path.join(CSRC, "kashin_api.cpp"), os.path.join(CSRC, "kashin_dispatch.hip")]
+    srcs = [os.path.join(CSRC, "kashin_api.cpp"), os.path.join(CSRC, "kashin_dispatch.hip"),
+            os.path.join(CSRC, "kashin_rotate.hip")]
     srcs += sorted(glob.glob(os.path.join(CSRC, "kashin_n*.hip")))
     return srcs
 

@@ -310,6 +310,28 @@ int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void
   return launch(plan, a, (m + 1) / 2, stream);
 }
 
+int kashin_rotate(int32_t n, uint64_t seed, int32_t inverse, const void* x, int32_t dtype, int64_t m, int64_t ldx,
+                  float* y, int64_t ldy, void* stream) {
+  if (!kashin::rotate_supported_n(n))
+    return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", n);
+  if (inverse != 0 && inverse != 1) return fail(KASHIN_E_INVALID, "inverse must be 0 or 1");
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (m < 0) return fail(KASHIN_E_INVALID, "m must be >= 0 (got %lld)", (long long)m);
+  if (ldx < n || ldy < n) return fail(KASHIN_E_INVALID, "ldx (%lld) and ldy (%lld) must be >= n (%d)", (long long)ldx,
+                                      (long long)ldy, n);
+  if (m == 0) return ok();
+  if (!x || !y) return fail(KASHIN_E_INVALID, "x and y must be non-null");
+  const size_t esz = dtype == KASHIN_F16 ? 2 : 4;
+  const uintptr_t x0 = reinterpret_cast<uintptr_t>(x), y0 = reinterpret_cast<uintptr_t>(y);
+  const uintptr_t x1 = x0 + ((m - 1) * ldx + n) * esz, y1 = y0 + ((m - 1) * ldy + n) * 4;
+  const bool in_place = x0 == y0 && dtype == KASHIN_F32 && ldx == ldy;
+  if (!in_place && x0 < y1 && y0 < x1) return fail(KASHIN_E_INVALID, "x and y overlap without being the same rows");
+  const hipError_t e =
+      kashin::launch_rotate(n, seed, inverse != 0, x, dtype, ldx, y, ldy, m, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return ok();
+}
+
 int kashin_reconstruct(kashin_plan_t plan, const uint8_t* codes_u, const uint8_t* codes_v, const float* centers,
                        int64_t m, float* w_hat, int64_t ldw, void* stream) {
   int st = check_common(plan, m);

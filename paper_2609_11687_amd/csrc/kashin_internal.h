@@ -74,4 +74,9 @@ bool supported_n(int n);
 hipError_t launch_pair(int n, const KArgs& a, int64_t grid, hipStream_t stream);
 hipError_t launch_cluster(const ClusterArgs& a, hipStream_t stream);
 
+// Incoherence rotation of rows (kashin_rotate.hip).
+bool rotate_supported_n(int n);
+hipError_t launch_rotate(int n, uint64_t seed, bool inverse, const void* x, int dtype, int64_t ldx, float* y,
+                         int64_t ldy, int64_t m, hipStream_t stream);
+
 }  // namespace kashin

@@ -24,7 +24,8 @@ KASHIN_F16 = 1
 EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
-    "kashin_quantize", "kashin_apply_p", "kashin_trace", "kashin_status_string", "kashin_last_error",
+    "kashin_quantize", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_status_string",
+    "kashin_last_error",
 )
 
 _lib = None
@@ -57,6 +58,7 @@ def lib() -> ctypes.CDLL:
         "kashin_reconstruct": [vp, vp, vp, vp, i64, vp, i64, vp],
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
+        "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
         "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
     }
     for name, args in sig.items():
@@ -191,6 +193,16 @@ def kashin_quantize(plan, w, lloyd_iters, codes_u, codes_v, centers, stream=None
 def kashin_apply_p(plan, x, y, stream=None):
     m = x.shape[0]
     _check(lib().kashin_apply_p(plan.handle, _ptr(x), _ptr(y), m, _stream(stream)))
+
+
+def kashin_rotate(n, seed, x, y, inverse=False, stream=None):
+    """y = R x (or R^T x) row-wise; x fp32 or fp16 rows, y fp32 rows (y may be x, fp32)."""
+    m, ldx = _rows(x)
+    my, ldy = _rows(y)
+    if my != m:
+        raise ValueError("x and y must have the same number of rows")
+    _check(lib().kashin_rotate(n, seed, 1 if inverse else 0, _ptr(x), _dtype_code(x), m, ldx, _ptr(y), ldy,
+                               _stream(stream)))
 
 
 def kashin_trace(plan, w, rows, sign_trace, c_trace, u, vhat, stream=None):

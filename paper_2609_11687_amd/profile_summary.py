@@ -27,9 +27,13 @@ COPY_BYTES = 256 << 20  # the calibration copy reads and writes 256 MiB
 
 
 def _short(name: str) -> tuple[str, int]:
-    m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|cluster_kernel|__amd_rocclr_copyBuffer\w*|elementwise_kernel)", name)
+    m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|rotate_kernel|cluster_kernel|__amd_rocclr_copyBuffer\w*|"
+                  r"elementwise_kernel)", name)
     c = re.search(r"Cfg<(\d+)", name)
     base = m.group(1) if m else name[:40]
+    rot = re.search(r"rotate_kernel<(\d+), (true|false)", name)  # rotate_kernel<odd factor, inverse, input type>
+    if rot:
+        base += f"[b={rot.group(1)}" + (",inverse]" if rot.group(2) == "true" else "]")
     flags = re.search(r">, (true|false), (true|false)>", name)  # pair_greedy_kernel<Cfg, LLOYD, QUANT>
     if flags:
         base += ("[quantize" + (",lloyd" if flags.group(1) == "true" else "") + "]"
@@ -107,7 +111,7 @@ def main() -> int:
             k, n, wg, wx = key
             b = fetch[key] * 1024 * f_fac + write[key] * 1024 * w_fac
             out.append(f"  {k:28s} {n:6d} {wg:6d} {fetch[key]:11.1f} {write[key]:11.1f} {b:12.4g}")
-            if k.startswith("pair_"):
+            if k.startswith(("pair_", "rotate_")):
                 traffic["bytes"][f"{k}|{n}/{wg}"] = b
     print("\n".join(out))
     if traffic is not None:

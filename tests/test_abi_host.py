@@ -89,3 +89,25 @@ def test_plan_needs_a_device_or_succeeds():
         assert L.kashin_plan_destroy(h) == K.KASHIN_OK
     else:
         assert st == K.KASHIN_E_HIP
+
+
+def test_rotate_validation_before_device():
+    """kashin_rotate rejects bad sizes, dtypes, strides and overlapping buffers on the host;
+    m = 0 is a no-op (pointers are never dereferenced)."""
+    L = K.lib()
+    x = ctypes.c_void_p(0x10000)
+    y = ctypes.c_void_p(0x90000)
+    assert L.kashin_rotate(320, 0, 0, x, 0, 4, 320, y, 320, None) == K.KASHIN_E_UNSUPPORTED_N  # odd part 5
+    assert L.kashin_rotate(32768, 0, 0, x, 0, 4, 32768, y, 32768, None) == K.KASHIN_E_UNSUPPORTED_N
+    assert L.kashin_rotate(512, 0, 2, x, 0, 4, 512, y, 512, None) == K.KASHIN_E_INVALID
+    assert L.kashin_rotate(512, 0, 0, x, 7, 4, 512, y, 512, None) == K.KASHIN_E_INVALID
+    assert L.kashin_rotate(512, 0, 0, x, 0, -1, 512, y, 512, None) == K.KASHIN_E_INVALID
+    assert L.kashin_rotate(512, 0, 0, x, 0, 4, 511, y, 512, None) == K.KASHIN_E_INVALID
+    assert L.kashin_rotate(512, 0, 0, x, 0, 4, 512, y, 500, None) == K.KASHIN_E_INVALID
+    assert L.kashin_rotate(512, 0, 0, None, 0, 4, 512, y, 512, None) == K.KASHIN_E_INVALID
+    # y starts inside x's rows without being the same rows
+    assert L.kashin_rotate(512, 0, 0, x, 0, 4, 512, ctypes.c_void_p(0x10000 + 64), 512, None) == K.KASHIN_E_INVALID
+    # in place is allowed only for fp32 rows with equal strides
+    assert L.kashin_rotate(512, 0, 0, x, 1, 4, 512, x, 512, None) == K.KASHIN_E_INVALID
+    assert "overlap" in L.kashin_last_error().decode()
+    assert L.kashin_rotate(11008, 0, 1, x, 0, 0, 11008, y, 11008, None) == K.KASHIN_OK

@@ -424,3 +424,79 @@ def test_stack_first_and_last_layer():
             total_codes += tot
     _say(f"llama7b_stack: code mismatches {total_m} of {total_codes}")
     assert total_m <= max(1, int(1e-4 * total_codes))
+
+
+# ----------------------------------------------------------------------------- incoherence rotation
+@pytest.mark.parametrize("n", ALL_N)
+def test_rotate_matches_oracle(n):
+    """y = R x and x = R^T y against the oracle's dense R, fp32 rows; fp16 input equals fp32
+    input of the same values bit for bit; in place equals out of place bit for bit."""
+    rng = np.random.default_rng(3 * n)
+    seed = 77 + n
+    m = 5
+    x = _rows(rng, m, n, "outlier")
+    xd = pu.to_dev(x)
+    y = torch.empty_like(xd)
+    K.kashin_rotate(n, seed, xd, y)
+    back = torch.empty_like(xd)
+    K.kashin_rotate(n, seed, y, back, inverse=True)
+    yh = torch.empty_like(xd)
+    xh = xd.half()
+    K.kashin_rotate(n, seed, xh, yh)
+    yf = torch.empty_like(xd)
+    K.kashin_rotate(n, seed, xh.float(), yf)
+    inplace = xd.clone()
+    K.kashin_rotate(n, seed, inplace, inplace)
+    torch.cuda.synchronize()
+    yref = ref.rotate(x.astype(np.float64), seed)
+    scale = max(np.abs(x).max(), np.abs(yref).max())
+    err = np.abs(y.cpu().numpy() - yref).max() / scale
+    inv_err = np.abs(back.cpu().numpy() - x).max() / scale
+    _say(f"rotate N={n}: max err / scale = {err:.2e}, round trip {inv_err:.2e}")
+    assert err <= 2e-6
+    assert inv_err <= 4e-6
+    yinv_ref = ref.rotate(x.astype(np.float64), seed, inverse=True)
+    yinv = torch.empty_like(xd)
+    K.kashin_rotate(n, seed, xd, yinv, inverse=True)
+    torch.cuda.synchronize()
+    assert np.abs(yinv.cpu().numpy() - yinv_ref).max() / scale <= 2e-6
+    np.testing.assert_array_equal(yh.cpu().numpy(), yf.cpu().numpy())
+    np.testing.assert_array_equal(inplace.cpu().numpy(), y.cpu().numpy())
+
+
+def test_rotated_quantization_pipeline():
+    """The +H composition on full llama7b matrices (q_proj, down_proj; fp16 rows): R w on the
+    GPU, quantised, reconstructed and rotated back.  Sampled rows: R w against the oracle, and
+    w_hat against the oracle's R^T (u_q + P v_q) from the same codes and centres."""
+    wl = synth.WORKLOADS["llama7b"]
+    names = [s.name for s in wl.matrices]
+    rot_seed = 1234
+    for name in ("q_proj", "down_proj"):
+        idx = names.index(name)
+        spec = wl.matrices[idx]
+        seed = synth.sign_seed(wl, 0, idx)
+        w = synth.make_matrix(wl, 0, idx)
+        wd = pu.to_dev(w).to(torch.float16)
+        wr = torch.empty((spec.rows, spec.n), dtype=torch.float32, device="cuda")
+        K.kashin_rotate(spec.n, rot_seed, wd, wr)
+        plan = K.kashin_plan(spec.n, seed, wl.iters)
+        cu, cv, ce = K.quantize_alloc(plan, wr, 0)
+        wh = torch.empty_like(wr)
+        K.kashin_reconstruct(plan, cu, cv, ce, wh)
+        K.kashin_rotate(spec.n, rot_seed, wh, wh, inverse=True)
+        torch.cuda.synchronize()
+        rows = [0, 3, spec.rows // 2, spec.rows - 1]
+        w64 = w[rows].astype(np.float64)
+        rref = ref.rotate(w64, rot_seed)
+        rerr = np.abs(wr.cpu().numpy()[rows] - rref).max() / np.abs(rref).max()
+        cu_s = pu.unpack(cu.cpu().numpy()[rows], spec.n)
+        cv_s = pu.unpack(cv.cpu().numpy()[rows], spec.n)
+        ce_s = ce.cpu().numpy()[rows].astype(np.float64)
+        whref = ref.rotate(ref.reconstruct(cu_s, cv_s, ce_s, ref.sign_mask(spec.n, seed)), rot_seed, inverse=True)
+        herr = np.abs(wh.cpu().numpy()[rows] - whref).max() / np.abs(whref).max()
+        rel = np.linalg.norm(wh.cpu().numpy()[rows] - w64) / np.linalg.norm(w64)
+        _say(f"+H {name} N={spec.n}: rotate err {rerr:.2e}, w_hat err {herr:.2e}, "
+             f"relative reconstruction error {rel:.3f}")
+        assert rerr <= 2e-6
+        assert herr <= 1e-5
+        del plan

@@ -394,3 +394,45 @@ def test_replay_negative_tau_is_plain_run(rng):
     rep = ref.decompose(w, eps, 2, replay_signs=junk, tau=np.array([-1.0, -1.0]))
     np.testing.assert_array_equal(rep["u"], base["u"])
     assert not rep["replay_outside"].any()
+
+
+# ----------------------------------------------------------------------------- incoherence rotation
+@pytest.mark.parametrize("m", [1, 2, 4, 8, 16, 64, 256])
+def test_hadamard_matches_library(m):
+    """Sylvester construction against scipy's Hadamard matrix."""
+    import scipy.linalg
+
+    np.testing.assert_array_equal(ref.hadamard_matrix(m), scipy.linalg.hadamard(m))
+
+
+@pytest.mark.parametrize("n", [64, 96, 172, 256, 768])
+def test_rotation_against_library_kronecker(n, rng):
+    """R x computed with library routines on the (2^a, b) reshaping of the signed row: scipy's
+    Hadamard matrix along the first axis, scipy's orthonormal DCT-II along the second (this pins
+    the Kronecker index order n = i b + j and the odd factor), then R^T undoes it and R is
+    orthogonal."""
+    import scipy.fft
+    import scipy.linalg
+
+    seed = 21 + n
+    p2 = n & -n
+    b = n // p2
+    x = rng.standard_normal((3, n))
+    xs = (x * ref.sign_mask(n, seed)[None, :]).reshape(3, p2, b)
+    y = np.einsum("ik,bkj->bij", scipy.linalg.hadamard(p2) / np.sqrt(p2), xs)
+    if b > 1:
+        y = scipy.fft.dct(y, type=2, norm="ortho", axis=2)
+    np.testing.assert_allclose(ref.rotate(x, seed), y.reshape(3, n), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ref.rotate(ref.rotate(x, seed), seed, inverse=True), x, rtol=0, atol=1e-12)
+    r = ref.rotation_matrix(n, seed)
+    np.testing.assert_allclose(r @ r.T, np.eye(n), rtol=0, atol=1e-12)
+
+
+def test_rotation_spreads_a_single_outlier():
+    """Incoherence: for n a power of two a one-hot row becomes a row of +-1/sqrt(n) (every
+    Hadamard entry has that magnitude), so an outlier's energy is spread over all entries."""
+    n = 256
+    e = np.zeros((1, n))
+    e[0, 37] = 5.0
+    y = ref.rotate(e, 3)
+    np.testing.assert_allclose(np.abs(y), 5.0 / np.sqrt(n), rtol=1e-14)
