@@ -32,6 +32,12 @@ of Language Models"):
 * ``optimal4_sse`` -- exact optimum of 1-D 4-level clustering (brute force over
   contiguous partitions of the sorted values, or an O(4 n^2) dynamic program),
   used to pin the clustering.
+* ``decompose_schedule`` -- the same greedy over the dictionary Q_N u P Q_N with
+  other step schedules: Alg. 2's blocks in reverse order (Sec. 4.2), the
+  adaptive choice of the half with the larger l1 correlation at every step
+  (the single-step global greedy selection the paper contrasts with Alg. 2),
+  and the original vector greedy of App. B (Alg. 1: that choice, with the
+  step the orthogonal projection onto the sign vector).
 * ``hadamard_matrix`` / ``rotation_matrix`` / ``rotate`` -- the incoherence
   pre-rotation applied to weight rows before the decomposition (the "+H"
   preprocessing of Sec. 5; the paper only names a QuIP-style randomised
@@ -75,6 +81,8 @@ __all__ = [
     "hadamard_matrix",
     "rotation_matrix",
     "rotate",
+    "SCHEDULES",
+    "decompose_schedule",
 ]
 
 _MASK64 = (1 << 64) - 1
@@ -472,4 +480,100 @@ def rotate(x: np.ndarray, seed: int, inverse: bool = False) -> np.ndarray:
     x = np.asarray(x, dtype=np.float64)
     r = rotation_matrix(x.shape[1], seed)
     return x @ r if inverse else x @ r.T
+
+
+# ---------------------------------------------------------------------------
+# Step schedules of the greedy over Q_N u P Q_N (Sec. 4.2; App. B, Alg. 1).
+# ---------------------------------------------------------------------------
+SCHEDULES = ("alternating", "reverse", "adaptive", "original")
+
+
+def decompose_schedule(w, eps, nsteps, schedule, *, tol=0.0, replay_signs=None, replay_choices=None,
+                       tau=None, choice_band=0.0):
+    """Greedy decomposition x = u + P vhat + r with ``nsteps`` atomic steps in the given schedule.
+
+    alternating  blocks (u, u, vhat, vhat): Alg. 2 (equals ``decompose`` for nsteps = 4k)
+    reverse      blocks (vhat, vhat, u, u): the reverse order named in Sec. 4.2
+    adaptive     every step takes the u-half when ||rho||_1 > ||P rho||_1, else the vhat-half,
+                 step size ||.||_1 / N (greedy selection over the whole dictionary)
+    original     Alg. 1 (App. B): the same choice, the step the orthogonal projection of the
+                 current vector onto its sign vector s (coefficient <x, s> / <s, s>); a row stops
+                 (takes no further steps) once ||rho||_2 < tol.
+    A u-step on rho: Delta = c sign(rho), u += Delta, rho -= Delta.  A vhat-step on x = P rho:
+    Delta = c sign(x), vhat += Delta, rho -= P Delta.
+
+    Replay, as in ``decompose``: ``replay_signs`` (B, nsteps, n) and ``tau`` (B,) settle sign
+    decisions on entries with |x_i| <= tau while c >= tau; ``replay_choices`` (B, nsteps) int8
+    (0 u, 1 vhat) settles the adaptive choice when | ||rho||_1 - ||P rho||_1 | <= choice_band
+    (||rho||_1 + ||P rho||_1); a given choice outside that band that differs from the oracle's
+    is counted in ``choice_outside``.
+    Trace: ``choice`` (B, nsteps) int8 (0 u, 1 vhat, -1 stopped), ``c``, ``l1u`` = ||rho||_1,
+    ``l1v`` = ||P rho||_1 before the step, ``r2`` = ||rho||_2^2 after it, ``signs``.
+    """
+    if schedule not in SCHEDULES:
+        raise ValueError(f"schedule must be one of {SCHEDULES}")
+    w = np.array(w, dtype=np.float64, copy=True)
+    if w.ndim == 1:
+        w = w[None, :]
+    bsz, n = w.shape
+    rho = w.copy()
+    u = np.zeros_like(w)
+    vhat = np.zeros_like(w)
+    tr = {"choice": np.zeros((bsz, nsteps), dtype=np.int8), "c": np.zeros((bsz, nsteps)),
+          "l1u": np.zeros((bsz, nsteps)), "l1v": np.zeros((bsz, nsteps)), "r2": np.zeros((bsz, nsteps)),
+          "signs": np.zeros((bsz, nsteps, n), dtype=np.int8)}
+    outside = np.zeros(bsz, dtype=np.int64)
+    choice_outside = np.zeros(bsz, dtype=np.int64)
+    if replay_signs is not None:
+        tau = np.broadcast_to(np.asarray(tau, dtype=np.float64), (bsz,))
+    for step in range(nsteps):
+        xu = rho
+        xv = apply_p(rho, eps)
+        l1u = np.abs(xu).sum(axis=1)
+        l1v = np.abs(xv).sum(axis=1)
+        pos = step % 4
+        if schedule == "alternating":
+            take_v = np.full(bsz, pos >= 2)
+        elif schedule == "reverse":
+            take_v = np.full(bsz, pos < 2)
+        else:
+            take_v = ~(l1u > l1v)
+            if replay_choices is not None:
+                given = np.asarray(replay_choices)[:, step] == 1
+                band = np.abs(l1u - l1v) <= choice_band * (l1u + l1v)
+                choice_outside += (~band & (given != take_v)).astype(np.int64)
+                take_v = np.where(band, given, take_v)
+        active = np.ones(bsz, dtype=bool)
+        if schedule == "original" and tol > 0:
+            active = np.sqrt((rho * rho).sum(axis=1)) >= tol
+        x = np.where(take_v[:, None], xv, xu)
+        l1 = np.where(take_v, l1v, l1u)
+        s = np.sign(x)
+        c0 = l1 / n
+        if replay_signs is not None:
+            gs = replay_signs[:, step, :].astype(np.float64)
+            live = ((c0 >= tau) & (tau >= 0))[:, None]
+            band = live & (np.abs(x) <= tau[:, None])
+            outside += (live & ~band & (gs != s)).sum(axis=1)
+            s = np.where(band, gs, s)
+        if schedule == "original":
+            ss = (s * s).sum(axis=1)
+            c = np.where(ss > 0, (x * s).sum(axis=1) / np.maximum(ss, 1), 0.0)
+        else:
+            c = c0
+        c = np.where(active, c, 0.0)
+        d = s * c[:, None]
+        du = np.where(take_v[:, None], 0.0, d)
+        dv = np.where(take_v[:, None], d, 0.0)
+        u += du
+        vhat += dv
+        rho = rho - du - apply_p(dv, eps)
+        tr["choice"][:, step] = np.where(active, take_v.astype(np.int8), -1)
+        tr["c"][:, step] = c
+        tr["l1u"][:, step] = l1u
+        tr["l1v"][:, step] = l1v
+        tr["r2"][:, step] = (rho * rho).sum(axis=1)
+        tr["signs"][:, step] = s.astype(np.int8)
+    return {"u": u, "vhat": vhat, "r": rho, "trace": tr, "replay_outside": outside,
+            "choice_outside": choice_outside}
 

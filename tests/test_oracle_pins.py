@@ -436,3 +436,88 @@ def test_rotation_spreads_a_single_outlier():
     e[0, 37] = 5.0
     y = ref.rotate(e, 3)
     np.testing.assert_allclose(np.abs(y), 5.0 / np.sqrt(n), rtol=1e-14)
+
+
+# ----------------------------------------------------------------------------- step schedules
+def test_alternating_schedule_is_alg2(rng):
+    n = 48
+    eps = ref.sign_mask(n, 4)
+    w = rng.standard_normal((3, n))
+    a = ref.decompose(w, eps, 4)
+    b = ref.decompose_schedule(w, eps, 16, "alternating")
+    np.testing.assert_array_equal(a["u"], b["u"])
+    np.testing.assert_array_equal(a["vhat"], b["vhat"])
+
+
+def test_reverse_schedule_is_alternating_on_p_w(rng):
+    """A vhat-step on P rho is a u-step on rho' = P rho and vice versa (P^2 = I), so the reverse
+    schedule on w is the alternating schedule on P w with the factors exchanged and r -> P r."""
+    n = 40
+    eps = ref.sign_mask(n, 6)
+    w = rng.standard_normal((2, n))
+    rev = ref.decompose_schedule(w, eps, 12, "reverse")
+    alt = ref.decompose_schedule(ref.apply_p(w, eps), eps, 12, "alternating")
+    np.testing.assert_allclose(rev["u"], alt["vhat"], atol=1e-12)
+    np.testing.assert_allclose(rev["vhat"], alt["u"], atol=1e-12)
+    np.testing.assert_allclose(rev["r"], ref.apply_p(alt["r"], eps), atol=1e-12)
+
+
+@pytest.mark.parametrize("schedule", ["reverse", "adaptive", "original"])
+def test_schedule_energy_identity_and_reconstruction(schedule, rng):
+    """Every step of every schedule removes exactly 2 c <x, s> - c^2 <s, s> of ||rho||^2 (x the
+    stepped vector, rho or P rho, s its sign vector; P is orthogonal), and x = u + P vhat + r."""
+    n = 56
+    eps = ref.sign_mask(n, 8)
+    w = rng.standard_normal((3, n))
+    d = ref.decompose_schedule(w, eps, 24, schedule)
+    tr = d["trace"]
+    r2_prev = (w * w).sum(axis=1)
+    rho = w.copy()
+    for s in range(24):
+        take_v = tr["choice"][:, s] == 1
+        xs = np.where(take_v[:, None], ref.apply_p(rho, eps), rho)
+        sg = tr["signs"][:, s].astype(np.float64)
+        c = tr["c"][:, s]
+        drop = 2 * c * (xs * sg).sum(axis=1) - c * c * (sg * sg).sum(axis=1)
+        np.testing.assert_allclose(r2_prev - tr["r2"][:, s], drop, rtol=1e-10, atol=1e-12)
+        dlt = sg * c[:, None]
+        rho = rho - np.where(take_v[:, None], ref.apply_p(dlt, eps), dlt)
+        r2_prev = tr["r2"][:, s]
+    np.testing.assert_allclose(w, d["u"] + ref.apply_p(d["vhat"], eps) + d["r"], atol=1e-12)
+
+
+def test_adaptive_takes_the_larger_decrease(rng):
+    """With no zero entries the decrease of a step of size ||x||_1 / N is ||x||_1^2 / N, so the
+    adaptive choice (the larger l1) is the larger of the two possible decreases."""
+    n = 64
+    eps = ref.sign_mask(n, 9)
+    w = rng.standard_normal((4, n))
+    d = ref.decompose_schedule(w, eps, 16, "adaptive")
+    tr = d["trace"]
+    r2_prev = (w * w).sum(axis=1)
+    for s in range(16):
+        best = np.maximum(tr["l1u"][:, s], tr["l1v"][:, s]) ** 2 / n
+        np.testing.assert_allclose(r2_prev - tr["r2"][:, s], best, rtol=1e-10)
+        r2_prev = tr["r2"][:, s]
+
+
+def test_original_step_is_an_orthogonal_projection(rng):
+    """Alg. 1's step projects the stepped vector onto its sign vector: afterwards the vector is
+    orthogonal to that sign vector, and rows stop once ||rho||_2 < tol."""
+    n = 32
+    eps = ref.sign_mask(n, 10)
+    w = rng.standard_normal((2, n))
+    w[0, :5] = 0.0  # zeros: the projection divides by nnz, not by n
+    d = ref.decompose_schedule(w, eps, 30, "original", tol=1e-3)
+    tr = d["trace"]
+    rho = w.copy()
+    for s in range(30):
+        take_v = tr["choice"][:, s] == 1
+        xs = np.where(take_v[:, None], ref.apply_p(rho, eps), rho)
+        sg = tr["signs"][:, s].astype(np.float64)
+        dlt = sg * tr["c"][:, s][:, None]
+        live = tr["choice"][:, s] >= 0
+        np.testing.assert_allclose(((xs - dlt) * sg).sum(axis=1)[live], 0.0, atol=1e-12)
+        rho = rho - np.where(take_v[:, None], ref.apply_p(dlt, eps), dlt)
+    assert (tr["choice"][:, -1] == -1).all()  # both rows reached the tolerance
+    assert (np.sqrt((d["r"] ** 2).sum(axis=1)) < 1e-3).all()
