@@ -14,6 +14,8 @@
   workload, fp16 rows in, fp32 rows out.
 --op quantize_h: one step = the "+H" pipeline, R w followed by kashin_quantize of the rotated
   rows, for every matrix of the workload.
+--op schedule: one step = kashin_decompose_schedule (--schedule alternating | reverse | adaptive |
+  original) over every matrix of the workload, 4k atomic steps, factors and residual written.
 """
 from __future__ import annotations
 
@@ -35,6 +37,7 @@ METRIC_APPLY_P = "activation rows transformed/s (y = P x, fp32); % of HBM roofli
 METRIC_RECON = "weight rows reconstructed/s (w_hat = u_q + P v_q from 2+2-bit codes, fp32 out); % of HBM roofline"
 METRIC_ROTATE = "weight rows rotated/s (R w, fp16 in, fp32 out); % of HBM roofline"
 METRIC_QUANT_H = "weight vectors rotated + decomposed + quantised/s (+H pipeline, N=4096, fixed iters)"
+METRIC_SCHED = "weight vectors decomposed/s with the {} step schedule (4k steps, both residual domains kept)"
 ROT_SEED = 1234  # seed of the rotation's sign vector
 PEAK_FP32_TFLOPS = 157.3   # MI355X published FP32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
 PEAK_HBM_GBPS = 8000.0     # MI355X published HBM3E bandwidth
@@ -207,8 +210,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
-    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h"),
+    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h", "schedule"),
                     default="quantize")
+    ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
@@ -244,7 +248,7 @@ def main() -> int:
     launches: list[Launch] = []
     keep = []  # device buffers and plans referenced by the launches
 
-    if args.op in ("quantize", "reconstruct", "rotate", "quantize_h"):
+    if args.op in ("quantize", "reconstruct", "rotate", "quantize_h", "schedule"):
         for layer in range(wl.layers):
             for idx, spec in enumerate(wl.matrices):
                 log(f"generating {args.workload} layer {layer} {spec.name} {spec.rows}x{spec.n}")
@@ -257,7 +261,17 @@ def main() -> int:
                 cu = torch.empty((spec.rows, nb), dtype=torch.uint8, device=dev)
                 cv = torch.empty_like(cu)
                 ce = torch.empty((spec.rows, 2, 4), dtype=torch.float32, device=dev)
-                if args.op in ("rotate", "quantize_h"):
+                if args.op == "schedule":
+                    uu = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
+                    vv, rr_ = torch.empty_like(uu), torch.empty_like(uu)
+                    keep.append((plan, wd, uu, vv, rr_))
+                    launches.append(Launch(
+                        spec.n, spec.rows, spec.rows * 2 * (4 * wl.iters + 2) * transform_flops(spec.n),
+                        spec.rows * (spec.n * (2 if spec.dtype == "f16" else 4) + 12 * spec.n),
+                        lambda s, a=(plan, wd, uu, vv, rr_): K.kashin_decompose_schedule(
+                            a[0], args.schedule, a[1], a[2], a[3], a[4], stream=s),
+                        kind="schedule"))
+                elif args.op in ("rotate", "quantize_h"):
                     wr = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
                     keep.append((plan, wd, wr, cu, cv, ce))
                     p2 = spec.n & -spec.n
@@ -308,14 +322,27 @@ def main() -> int:
     by_n, per_n = per_n_figures(launches, launch_ms)
 
     # dominant kernel: the N = 4096 launches (if present) of the op's main kernel, averaged over them
-    main_kind = {"quantize": "quantize", "quantize_h": "quantize", "rotate": "rotate"}.get(args.op, "pmap")
+    main_kind = {"quantize": "quantize", "quantize_h": "quantize", "rotate": "rotate",
+                 "schedule": "schedule"}.get(args.op, "pmap")
     dom_n = 4096 if 4096 in by_n else max(by_n, key=lambda n: by_n[n]["ms"])
     dom = [(l, ms) for l, ms in zip(launches, launch_ms) if l.n == dom_n and l.kind == main_kind]
     dom_s = sum(ms for _, ms in dom) / 1e3
     dom_flops = sum(l.flops for l, _ in dom)
     dom_bytes = sum(l.nbytes for l, _ in dom)
     layer = ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices) + f" x {wl.layers} layer(s)"
-    if main_kind == "quantize":
+    if main_kind == "schedule":
+        achieved = dom_flops / dom_s / 1e12
+        roofline = {
+            "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+            "kernel": f"pair_schedule_kernel N={dom_n}", "launches": len(dom),
+            "flops_per_vector": 2 * (4 * wl.iters + 2) * transform_flops(dom_n),
+            "algorithmic_bytes_per_launch": dom_bytes / len(dom),
+        }
+        metric, unit = METRIC_SCHED.format(args.schedule), "vectors/s"
+        workload = (f"{args.workload} {args.schedule} schedule: {layer}, {wl.matrices[0].dtype} storage, "
+                    f"{4 * wl.iters} atomic steps")
+    elif main_kind == "quantize":
         achieved = dom_flops / dom_s / 1e12
         roofline = {
             "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
@@ -376,6 +403,22 @@ def main() -> int:
         "roofline": roofline,
         "source_digest": source_digest(),
     }
+    if args.op == "schedule":
+        # convergence (Fig. 2 style): ||rho||_2 / ||w||_2 after 4, 8, 16 and 32 atomic steps, the
+        # mean over the first 8 rows of the first matrix (recorded by kashin_trace_schedule)
+        plan, wd, *_ = keep[0]
+        nr, n0, steps = 8, wd.shape[1], 4 * wl.iters
+        rows_t = torch.arange(nr, dtype=torch.int64, device=dev)
+        sg = torch.empty((nr, steps, n0), dtype=torch.int8, device=dev)
+        cs = torch.empty((nr, steps), dtype=torch.float32, device=dev)
+        ch = torch.empty((nr, steps), dtype=torch.int8, device=dev)
+        r2 = torch.empty((nr, steps), dtype=torch.float32, device=dev)
+        ut, vt = torch.empty((nr, n0), device=dev), torch.empty((nr, n0), device=dev)
+        K.kashin_trace_schedule(plan, args.schedule, wd, rows_t, sg, cs, ch, r2, ut, vt)
+        torch.cuda.synchronize()
+        w2 = (wd[:nr].float() ** 2).sum(dim=1)
+        result["convergence"] = {str(s_): (r2[:, s_ - 1] / w2).sqrt().mean().item() for s_ in (4, 8, 16, 32)
+                                 if s_ <= steps}
     if not args.no_cpu_baseline:
         if args.op == "quantize":
             log(f"cpu baseline: oracle on {args.cpu_rows} rows")

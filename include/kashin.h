@@ -110,6 +110,36 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
  * x and y may not alias. */
 int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream);
 
+/* Step schedules of the greedy over the dictionary Q_N u P Q_N (Sec. 4.2 and App. B). */
+enum {
+  KASHIN_SCHED_ALTERNATING = 0, /* blocks u, u, vhat, vhat: Alg. 2 */
+  KASHIN_SCHED_REVERSE = 1,     /* blocks vhat, vhat, u, u: the reverse order named in Sec. 4.2 */
+  KASHIN_SCHED_ADAPTIVE = 2,    /* every step: the u-half when ||rho||_1 > ||P rho||_1, else the
+                                   vhat-half, step ||.||_1 / N (greedy selection over the whole
+                                   dictionary, which Alg. 2 replaces) */
+  KASHIN_SCHED_ORIGINAL = 3     /* Alg. 1 (App. B): the same choice, the step the orthogonal
+                                   projection onto the sign vector (||.||_1 / nnz); a row takes
+                                   no further steps once ||rho||_2 < tol */
+};
+
+/* The decomposition w = u + P vhat + r with 4k atomic steps (k = the plan's iters) in the given
+ * schedule; sign(0) = 0 as in Alg. 2.  Layouts as kashin_decompose (r nullable).  Every step
+ * applies P once (both domains of the residual are kept), so a step costs twice the transforms
+ * of the alternating schedule of kashin_decompose.  tol applies to KASHIN_SCHED_ORIGINAL only
+ * (0: never stop early), in the units of w. */
+int kashin_decompose_schedule(kashin_plan_t plan, int32_t schedule, float tol, const void* w, int32_t dtype,
+                              int64_t m, int64_t ldw, float* u, float* vhat, float* r, void* stream);
+
+/* Replay record of kashin_decompose_schedule for the listed rows (as kashin_trace):
+ *   sign_trace    nrows x 4k x n int8, element order of w: sign taken in the stepped vector
+ *   c_trace       nrows x 4k fp32: step size
+ *   choice_trace  nrows x 4k int8: 0 u-step, 1 vhat-step, -1 stopped (KASHIN_SCHED_ORIGINAL)
+ *   r2_trace      nrows x 4k fp32: ||rho||_2^2 after the step
+ *   u, vhat       nrows x n fp32 factors (ld n). */
+int kashin_trace_schedule(kashin_plan_t plan, int32_t schedule, float tol, const void* w, int32_t dtype, int64_t m,
+                          int64_t ldw, const int64_t* rows, int64_t nrows, int8_t* sign_trace, float* c_trace,
+                          int8_t* choice_trace, float* r2_trace, float* u, float* vhat, void* stream);
+
 /* Incoherence pre-rotation of rows, the "+H" preprocessing of Sec. 5 (the paper names a
  * QuIP-style randomised Hadamard transform, with a Kronecker variant, applied to the weights
  * before the decomposition; it gives no construction, so this one is a reading):

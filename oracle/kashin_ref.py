@@ -504,9 +504,10 @@ def decompose_schedule(w, eps, nsteps, schedule, *, tol=0.0, replay_signs=None, 
 
     Replay, as in ``decompose``: ``replay_signs`` (B, nsteps, n) and ``tau`` (B,) settle sign
     decisions on entries with |x_i| <= tau while c >= tau; ``replay_choices`` (B, nsteps) int8
-    (0 u, 1 vhat) settles the adaptive choice when | ||rho||_1 - ||P rho||_1 | <= choice_band
-    (||rho||_1 + ||P rho||_1); a given choice outside that band that differs from the oracle's
-    is counted in ``choice_outside``.
+    (0 u, 1 vhat, -1 stopped) settles the adaptive choice when | ||rho||_1 - ||P rho||_1 | <=
+    choice_band (||rho||_1 + ||P rho||_1), and the stopping test of ``original`` when
+    | ||rho||_2 - tol | <= choice_band tol; a given decision outside its band that differs from the
+    oracle's is counted in ``choice_outside``.
     Trace: ``choice`` (B, nsteps) int8 (0 u, 1 vhat, -1 stopped), ``c``, ``l1u`` = ||rho||_1,
     ``l1v`` = ||P rho||_1 before the step, ``r2`` = ||rho||_2^2 after it, ``signs``.
     """
@@ -538,14 +539,20 @@ def decompose_schedule(w, eps, nsteps, schedule, *, tol=0.0, replay_signs=None, 
             take_v = np.full(bsz, pos < 2)
         else:
             take_v = ~(l1u > l1v)
-            if replay_choices is not None:
-                given = np.asarray(replay_choices)[:, step] == 1
-                band = np.abs(l1u - l1v) <= choice_band * (l1u + l1v)
-                choice_outside += (~band & (given != take_v)).astype(np.int64)
-                take_v = np.where(band, given, take_v)
         active = np.ones(bsz, dtype=bool)
         if schedule == "original" and tol > 0:
-            active = np.sqrt((rho * rho).sum(axis=1)) >= tol
+            norm = np.sqrt((rho * rho).sum(axis=1))
+            active = norm >= tol
+            if replay_choices is not None:
+                stopped = np.asarray(replay_choices)[:, step] == -1
+                band = np.abs(norm - tol) <= choice_band * tol
+                choice_outside += (~band & (stopped == active)).astype(np.int64)
+                active = np.where(band, ~stopped, active)
+        if schedule in ("adaptive", "original") and replay_choices is not None:
+            given = np.asarray(replay_choices)[:, step]
+            band = active & (given >= 0) & (np.abs(l1u - l1v) <= choice_band * (l1u + l1v))
+            choice_outside += (active & (given >= 0) & ~band & ((given == 1) != take_v)).astype(np.int64)
+            take_v = np.where(band, given == 1, take_v)
         x = np.where(take_v[:, None], xv, xu)
         l1 = np.where(take_v, l1v, l1u)
         s = np.sign(x)

@@ -295,6 +295,69 @@ int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, in
   return launch(plan, a, nrows, stream);
 }
 
+namespace {
+int check_schedule(int32_t schedule, float tol) {
+  if (schedule < KASHIN_SCHED_ALTERNATING || schedule > KASHIN_SCHED_ORIGINAL)
+    return fail(KASHIN_E_INVALID, "schedule must be one of KASHIN_SCHED_*");
+  if (!(tol >= 0.f)) return fail(KASHIN_E_INVALID, "tol must be >= 0");
+  return KASHIN_OK;
+}
+}  // namespace
+
+int kashin_decompose_schedule(kashin_plan_t plan, int32_t schedule, float tol, const void* w, int32_t dtype,
+                              int64_t m, int64_t ldw, float* u, float* vhat, float* r, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  st = check_schedule(schedule, tol);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (m == 0) return ok();
+  if (!w || !u || !vhat) return fail(KASHIN_E_INVALID, "w, u and vhat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_SCHEDULE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.u = u;
+  a.vhat = vhat;
+  a.r = r;
+  a.schedule = schedule;
+  a.tol = tol;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_trace_schedule(kashin_plan_t plan, int32_t schedule, float tol, const void* w, int32_t dtype, int64_t m,
+                          int64_t ldw, const int64_t* rows, int64_t nrows, int8_t* sign_trace, float* c_trace,
+                          int8_t* choice_trace, float* r2_trace, float* u, float* vhat, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  st = check_schedule(schedule, tol);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (nrows < 0) return fail(KASHIN_E_INVALID, "nrows must be >= 0");
+  if (nrows == 0 || m == 0) return ok();
+  if (!w || !rows || !sign_trace || !c_trace || !choice_trace || !r2_trace || !u || !vhat)
+    return fail(KASHIN_E_INVALID, "w, rows, the four traces, u and vhat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_SCHEDULE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.rows = rows;
+  a.nrows = nrows;
+  a.tr_signs = sign_trace;
+  a.tr_c = c_trace;
+  a.tr_choice = choice_trace;
+  a.tr_r2 = r2_trace;
+  a.u = u;
+  a.vhat = vhat;
+  a.schedule = schedule;
+  a.tol = tol;
+  return launch(plan, a, nrows, stream);
+}
+
 int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream) {
   int st = check_common(plan, m);
   if (st) return st;

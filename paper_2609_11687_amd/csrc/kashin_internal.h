@@ -13,6 +13,14 @@ enum Mode : int32_t {
   MODE_TRACE = 2,      // decompose listed rows and record every sign decision
   MODE_APPLY_P = 3,    // y = P x
   MODE_RECON = 4,      // w_hat = u_q + P v_q
+  MODE_SCHEDULE = 5,   // greedy with another step schedule (writes u, vhat, r; traces listed rows)
+};
+
+enum Schedule : int32_t {
+  SCHED_ALTERNATING = 0,  // blocks u, u, vhat, vhat (Alg. 2)
+  SCHED_REVERSE = 1,      // blocks vhat, vhat, u, u
+  SCHED_ADAPTIVE = 2,     // the half with the larger l1 correlation, step ||.||_1 / N
+  SCHED_ORIGINAL = 3,     // Alg. 1: that choice, projection step ||.||_1 / nnz, stop at ||rho|| < tol
 };
 
 // Everything a launch needs, passed to the kernel by value.
@@ -45,6 +53,11 @@ struct KArgs {
   int64_t nrows;
   int8_t* tr_signs;
   float* tr_c;
+  // MODE_SCHEDULE
+  int32_t schedule;
+  float tol;
+  int8_t* tr_choice;
+  float* tr_r2;
 };
 
 struct ClusterArgs {

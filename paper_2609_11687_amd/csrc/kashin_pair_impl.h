@@ -1425,6 +1425,182 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   }
 }
 
+// ------------------------------------------------------------------ schedule variants
+// The greedy over Q_N u P Q_N with another step schedule (MODE_SCHEDULE; a.schedule).  Both
+// domains of the residual are kept per row of the pair, rho and z = P rho; a step works in one
+// domain per row (the two rows of a pair may choose differently), and one application of P to
+// the pair's stepped values refreshes the other domain of both rows (P^2 = I).  That is one P
+// per atomic step, twice what the alternating kernel needs, and four live arrays: the
+// register budget is relaxed to two waves per SIMD where the workgroup allows it.
+// With a.rows set, workgroup i decomposes the pair holding row a.rows[i] and records that
+// row's signs, step sizes, choices and ||rho||^2 after every step.
+template <class C>
+__global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::T <= 512 ? 2 : C::W))) void
+pair_schedule_kernel(KArgs a, int64_t item0) {
+  __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
+  __shared__ float red[2 * C::NW * 32];
+  const int64_t item = item0 + blockIdx.x;
+  const bool tracing = a.rows != nullptr;
+  int64_t ra;
+  int side = 0;
+  if (tracing) {
+    const int64_t row = a.rows[item];
+    if (row < 0 || row >= a.m) return;  // uniform
+    ra = row & ~int64_t(1);
+    side = static_cast<int>(row & 1);
+  } else {
+    ra = 2 * item;
+  }
+  const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
+  int slot = 0;
+  constexpr bool RES = resident_ok<C>();
+  ResRegs<C> rr;
+  if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
+  auto applyP = [&](float2(&v)[C::E]) {
+    if constexpr (RES) apply_P_res<C>(v, lds, rr);
+    else apply_P<C>(v, lds, a.tw, a.mid4);
+  };
+  float2 rho[C::E], z[C::E], vh[C::E], y[C::E];
+  load_pair<C>(rho, a.w, a.dtype, a.ldw, ra, rb);
+  float2 scale, unscale;
+  bool bad_a, bad_b;
+  normalise_pair<C>(rho, red, slot, scale, unscale, bad_a, bad_b);
+#pragma unroll
+  for (int e = 0; e < C::E; ++e) {
+    z[e] = rho[e];
+    vh[e] = make_float2(0.f, 0.f);
+  }
+  applyP(z);
+  const int steps = 4 * a.iters;
+  const int sched = a.schedule;
+  const float tola = a.tol * scale.x, tolb = a.tol * scale.y;
+  const float unsel = side ? unscale.y : unscale.x;
+  for (int st = 0; st < steps; ++st) {
+    // l1 and nonzero counts of both domains, ||rho||^2, both rows
+    float v[10];
+#pragma unroll
+    for (int k = 0; k < 10; ++k) v[k] = 0.f;
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      v[0] += fabsf(rho[e].x);
+      v[1] += fabsf(rho[e].y);
+      v[2] += fabsf(z[e].x);
+      v[3] += fabsf(z[e].y);
+      v[4] += rho[e].x != 0.f ? 1.f : 0.f;
+      v[5] += rho[e].y != 0.f ? 1.f : 0.f;
+      v[6] += z[e].x != 0.f ? 1.f : 0.f;
+      v[7] += z[e].y != 0.f ? 1.f : 0.f;
+      v[8] += rho[e].x * rho[e].x;
+      v[9] += rho[e].y * rho[e].y;
+    }
+    block_sum<C::T, 10>(v, red, slot);
+    // threads past the last butterfly hold zeros: they add nothing to the counts above
+    const int pos = st & 3;
+    bool va, vb;  // true: the vhat-half (step on z)
+    if (sched == SCHED_ALTERNATING) {
+      va = vb = pos >= 2;
+    } else if (sched == SCHED_REVERSE) {
+      va = vb = pos < 2;
+    } else {
+      va = !(v[0] > v[2]);
+      vb = !(v[1] > v[3]);
+    }
+    const bool act_a = !(sched == SCHED_ORIGINAL && a.tol > 0.f && sqrtf(v[8]) < tola);
+    const bool act_b = !(sched == SCHED_ORIGINAL && a.tol > 0.f && sqrtf(v[9]) < tolb);
+    const float l1a = va ? v[2] : v[0], l1b = vb ? v[3] : v[1];
+    const float nza = va ? v[6] : v[4], nzb = vb ? v[7] : v[5];
+    float ca = sched == SCHED_ORIGINAL ? (nza > 0.f ? l1a / nza : 0.f) : div_n<C::N>(l1a);
+    float cb = sched == SCHED_ORIGINAL ? (nzb > 0.f ? l1b / nzb : 0.f) : div_n<C::N>(l1b);
+    ca = act_a ? ca : 0.f;
+    cb = act_b ? cb : 0.f;
+    if (tracing) {
+      const bool vs = side ? vb : va;
+      const int tid = opaque(static_cast<int>(threadIdx.x));
+      int8_t* trs = a.tr_signs + (item * steps + st) * int64_t(C::N);
+#pragma unroll
+      for (int i = 0; i < C::B0; ++i) {
+        const int j = tid + C::T * i;
+        if (j < C::NB0) {
+#pragma unroll
+          for (int r = 0; r < C::R0; ++r) {
+            const float2 xv = vs ? z[i * C::R0 + r] : rho[i * C::R0 + r];
+            trs[orig_index<C::N>(j + r * C::NB0)] = sgn8(side ? xv.y : xv.x);
+          }
+        }
+      }
+      if (threadIdx.x == 0) {
+        a.tr_c[item * steps + st] = (side ? cb : ca) * unsel;
+        a.tr_choice[item * steps + st] = (side ? act_b : act_a) ? (vs ? 1 : 0) : -1;
+      }
+    }
+    // the step, in each row's chosen domain; y collects the stepped values of both rows
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      float xa = va ? z[e].x : rho[e].x;
+      float xb = vb ? z[e].y : rho[e].y;
+      const float da = sgn_times(xa, ca), db = sgn_times(xb, cb);
+      xa -= da;
+      xb -= db;
+      if (va) {
+        vh[e].x += da;
+        z[e].x = xa;
+      } else {
+        rho[e].x = xa;
+      }
+      if (vb) {
+        vh[e].y += db;
+        z[e].y = xb;
+      } else {
+        rho[e].y = xb;
+      }
+      y[e] = make_float2(xa, xb);
+    }
+    applyP(y);  // the other domain of each row
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      if (va) rho[e].x = y[e].x;
+      else z[e].x = y[e].x;
+      if (vb) rho[e].y = y[e].y;
+      else z[e].y = y[e].y;
+    }
+    if (tracing) {
+      float q[1] = {0.f};
+#pragma unroll
+      for (int e = 0; e < C::E; ++e) q[0] += side ? rho[e].y * rho[e].y : rho[e].x * rho[e].x;
+      block_sum<C::T, 1>(q, red, slot);
+      if (threadIdx.x == 0) a.tr_r2[item * steps + st] = q[0] * unsel * unsel;
+    }
+  }
+  // u = w - P vhat - r (row reloaded from HBM)
+  const float qnan = __int_as_float(0x7fc00000);
+#pragma unroll
+  for (int e = 0; e < C::E; ++e) y[e] = vh[e];
+  applyP(y);
+  float2 t[C::E];
+  load_pair<C>(t, a.w, a.dtype, a.ldw, ra, rb);
+  int64_t oa = ra, ob = rb;
+  bool wa = true, wb = rb >= 0;
+  if (tracing) {
+    wa = side == 0;
+    wb = side == 1;
+    oa = ob = item;
+  }
+  for_each_elem<C>([&](int e, int i) {
+    const float ua = fmaf(t[e].x, scale.x, -rho[e].x) - y[e].x;
+    const float ub = fmaf(t[e].y, scale.y, -rho[e].y) - y[e].y;
+    if (wa) {
+      a.u[oa * C::N + i] = bad_a ? qnan : ua * unscale.x;
+      a.vhat[oa * C::N + i] = bad_a ? qnan : vh[e].x * unscale.x;
+      if (a.r != nullptr) a.r[oa * C::N + i] = bad_a ? qnan : rho[e].x * unscale.x;
+    }
+    if (wb) {
+      a.u[ob * C::N + i] = bad_b ? qnan : ub * unscale.y;
+      a.vhat[ob * C::N + i] = bad_b ? qnan : vh[e].y * unscale.y;
+      if (a.r != nullptr) a.r[ob * C::N + i] = bad_b ? qnan : rho[e].y * unscale.y;
+    }
+  });
+}
+
 // ------------------------------------------------------------------ dispatch
 template <class C>
 hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
@@ -1440,6 +1616,8 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
     } else if (a.mode <= MODE_TRACE) {
       hipLaunchKernelGGL((pair_greedy_kernel<C, false, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
                          i0);
+    } else if (a.mode == MODE_SCHEDULE) {
+      hipLaunchKernelGGL(pair_schedule_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
     } else {
       constexpr int64_t kPmapGrid = 2048;  // resident workgroups of the whole chip, a few times over
       const int64_t pg = g < kPmapGrid ? g : kPmapGrid;

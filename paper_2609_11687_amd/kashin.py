@@ -24,9 +24,10 @@ KASHIN_F16 = 1
 EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
-    "kashin_quantize", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_status_string",
-    "kashin_last_error",
+    "kashin_quantize", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
+    "kashin_trace_schedule", "kashin_status_string", "kashin_last_error",
 )
+SCHEDULES = {"alternating": 0, "reverse": 1, "adaptive": 2, "original": 3}
 
 _lib = None
 
@@ -59,6 +60,8 @@ def lib() -> ctypes.CDLL:
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
         "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
+        "kashin_decompose_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, vp, vp, vp],
+        "kashin_trace_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp],
         "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
     }
     for name, args in sig.items():
@@ -193,6 +196,20 @@ def kashin_quantize(plan, w, lloyd_iters, codes_u, codes_v, centers, stream=None
 def kashin_apply_p(plan, x, y, stream=None):
     m = x.shape[0]
     _check(lib().kashin_apply_p(plan.handle, _ptr(x), _ptr(y), m, _stream(stream)))
+
+
+def kashin_decompose_schedule(plan, schedule, w, u, vhat, r=None, tol=0.0, stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_decompose_schedule(plan.handle, SCHEDULES[schedule], tol, _ptr(w), _dtype_code(w), m, ldw,
+                                           _ptr(u), _ptr(vhat), _ptr(r), _stream(stream)))
+
+
+def kashin_trace_schedule(plan, schedule, w, rows, sign_trace, c_trace, choice_trace, r2_trace, u, vhat, tol=0.0,
+                          stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_trace_schedule(plan.handle, SCHEDULES[schedule], tol, _ptr(w), _dtype_code(w), m, ldw,
+                                       _ptr(rows), rows.numel(), _ptr(sign_trace), _ptr(c_trace), _ptr(choice_trace),
+                                       _ptr(r2_trace), _ptr(u), _ptr(vhat), _stream(stream)))
 
 
 def kashin_rotate(n, seed, x, y, inverse=False, stream=None):

@@ -500,3 +500,60 @@ def test_rotated_quantization_pipeline():
         assert rerr <= 2e-6
         assert herr <= 1e-5
         del plan
+
+
+# ----------------------------------------------------------------------------- step schedules
+SCHED_CASES = [(n, s) for n in (512, 4096, 11008) for s in ("alternating", "reverse", "adaptive", "original")]
+
+
+@pytest.mark.parametrize("n,schedule", SCHED_CASES)
+def test_schedule_replay_parity(n, schedule):
+    """kashin_decompose_schedule against the oracle's schedules: every row traced (signs, step
+    sizes, choices, ||rho||^2), the oracle replayed on the GPU's near-tie signs and near-tie
+    choices; decisions outside the bands must agree, factors within 1e-4 ||w||_inf, and
+    w = u + P vhat + r.  The traced factors equal the untraced call bit for bit."""
+    k = 5
+    steps = 4 * k
+    m = 5
+    rng = np.random.default_rng(17 * n + len(schedule))
+    w = _rows(rng, m, n, "t4")
+    seed = 300 + n
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, k)
+    wd = pu.to_dev(w)
+    tol = 0.05 * float(np.sqrt((w.astype(np.float64) ** 2).sum(axis=1)).min()) if schedule == "original" else 0.0
+    u = torch.empty_like(wd)
+    vh = torch.empty_like(wd)
+    r = torch.empty_like(wd)
+    K.kashin_decompose_schedule(plan, schedule, wd, u, vh, r, tol=tol)
+    rows_t = torch.arange(m, dtype=torch.int64, device="cuda")
+    sg = torch.empty((m, steps, n), dtype=torch.int8, device="cuda")
+    cs = torch.empty((m, steps), dtype=torch.float32, device="cuda")
+    ch = torch.empty((m, steps), dtype=torch.int8, device="cuda")
+    r2 = torch.empty((m, steps), dtype=torch.float32, device="cuda")
+    ut = torch.empty_like(wd)
+    vt = torch.empty_like(wd)
+    K.kashin_trace_schedule(plan, schedule, wd, rows_t, sg, cs, ch, r2, ut, vt, tol=tol)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ut.cpu().numpy(), u.cpu().numpy())
+    np.testing.assert_array_equal(vt.cpu().numpy(), vh.cpu().numpy())
+    w64 = w.astype(np.float64)
+    winf = np.abs(w64).max(axis=1)
+    rep = ref.decompose_schedule(w64, eps, steps, schedule, tol=tol, replay_signs=sg.cpu().numpy(),
+                                 replay_choices=ch.cpu().numpy(), tau=pu.TAU_REL * winf, choice_band=1e-5)
+    ug, vg, rg = (t.cpu().numpy().astype(np.float64) for t in (u, vh, r))
+    du = (np.abs(ug - rep["u"]).max(axis=1) / winf).max()
+    dv = (np.abs(vg - rep["vhat"]).max(axis=1) / winf).max()
+    rec = (np.abs(w64 - ug - ref.apply_p(vg, eps) - rg).max(axis=1) / winf).max()
+    gch = ch.cpu().numpy()
+    _say(f"schedule {schedule} N={n}: du={du:.2e} dv={dv:.2e} rec={rec:.2e} vhat-steps "
+         f"{(gch == 1).mean():.2f} stopped {(gch == -1).mean():.2f}")
+    assert not rep["replay_outside"].any(), "sign decisions outside the tie band disagree"
+    assert not rep["choice_outside"].any(), "step choices outside the tie band disagree"
+    np.testing.assert_array_equal(gch, rep["trace"]["choice"])
+    assert du <= pu.TOL_FACTOR and dv <= pu.TOL_FACTOR
+    assert rec <= pu.TOL_RECON
+    np.testing.assert_allclose(cs.cpu().numpy(), rep["trace"]["c"], rtol=1e-4, atol=1e-7 * winf.max())
+    np.testing.assert_allclose(r2.cpu().numpy(), rep["trace"]["r2"], rtol=1e-3, atol=1e-10 * (winf.max() ** 2) * n)
+    if schedule == "original":
+        assert (gch == -1).any()  # the tolerance stopped some rows
