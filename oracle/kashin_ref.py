@@ -38,6 +38,12 @@ of Language Models"):
   (the single-step global greedy selection the paper contrasts with Alg. 2),
   and the original vector greedy of App. B (Alg. 1: that choice, with the
   step the orthogonal projection onto the sign vector).
+* ``synthetic_hessian`` / ``optq_kashin`` -- the error-compensated pipeline of
+  Sec. 5 (Fig. 1): the columns of W are quantised chunk by chunk (Alg. 2 +
+  2-bit clustering on each column vector) and each chunk's error is carried
+  into the columns not yet quantised through the Cholesky factor of H^-1
+  (eq. optq_update, applied to a chunk at once); ``optq_reference`` is the
+  same compensation written with the explicit inverse-Hessian downdate.
 * ``hadamard_matrix`` / ``rotation_matrix`` / ``rotate`` -- the incoherence
   pre-rotation applied to weight rows before the decomposition (the "+H"
   preprocessing of Sec. 5; the paper only names a QuIP-style randomised
@@ -83,6 +89,9 @@ __all__ = [
     "rotate",
     "SCHEDULES",
     "decompose_schedule",
+    "synthetic_hessian",
+    "optq_kashin",
+    "optq_reference",
 ]
 
 _MASK64 = (1 << 64) - 1
@@ -583,4 +592,72 @@ def decompose_schedule(w, eps, nsteps, schedule, *, tol=0.0, replay_signs=None, 
         tr["signs"][:, step] = s.astype(np.int8)
     return {"u": u, "vhat": vhat, "r": rho, "trace": tr, "replay_outside": outside,
             "choice_outside": choice_outside}
+
+
+# ---------------------------------------------------------------------------
+# Error-compensated quantisation (Sec. 5, Fig. 1; eq. optq_update of App. on the stress tests).
+# ---------------------------------------------------------------------------
+def synthetic_hessian(d: int, nsamples: int, seed: int, outlier_cols: int = 0, outlier_scale: float = 1.0):
+    """H = X^T X / nsamples for seeded Gaussian activations X (nsamples, d); `outlier_cols`
+    channels scaled by `outlier_scale` (the activation outliers that make H ill-conditioned)."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((nsamples, d))
+    if outlier_cols:
+        x[:, rng.choice(d, outlier_cols, replace=False)] *= outlier_scale
+    return x.T @ x / nsamples
+
+
+def _damped(h, damp):
+    h = np.asarray(h, dtype=np.float64)
+    return h + damp * np.mean(np.diag(h)) * np.eye(h.shape[0])
+
+
+def _quantise_columns(cols, eps, k, lloyd_iters):
+    """Quantise each row of `cols` (one column vector of W per row) and dequantise it."""
+    cu, cv, centers, _ = quantize(cols, eps, k, lloyd_iters)
+    n = cols.shape[1]
+    return reconstruct(unpack2bit(cu, n), unpack2bit(cv, n), centers, eps), (cu, cv, centers)
+
+
+def optq_kashin(w, h, eps, k, chunk, damp=0.01, lloyd_iters=0):
+    """W (d_out, d_in), H (d_in, d_in): quantise the columns of W (vectors of length d_out) in
+    chunks of `chunk` columns; after each chunk c, with Delta = W_c - Q_c and U the upper Cholesky
+    factor of (H + damp mean(diag H) I)^-1, the remaining columns become W_r - Delta U_cc^-1 U_cr.
+    Returns (Q, W_final, codes) with codes = per chunk (codes_u, codes_v, centers)."""
+    w = np.array(w, dtype=np.float64, copy=True)
+    d_in = w.shape[1]
+    hinv = np.linalg.inv(_damped(h, damp))
+    u = np.linalg.cholesky(hinv).T  # hinv = u^T u, u upper triangular
+    q = np.zeros_like(w)
+    codes = []
+    for c0 in range(0, d_in, chunk):
+        c1 = min(c0 + chunk, d_in)
+        qc, cd = _quantise_columns(w[:, c0:c1].T, eps, k, lloyd_iters)
+        q[:, c0:c1] = qc.T
+        codes.append(cd)
+        delta = w[:, c0:c1] - q[:, c0:c1]
+        if c1 < d_in:
+            w[:, c1:] -= delta @ np.linalg.solve(u[c0:c1, c0:c1], u[c0:c1, c1:])
+    return q, w, codes
+
+
+def optq_reference(w, h, chunk, quantiser, damp=0.01):
+    """The same compensation written with the inverse Hessian of the remaining columns, downdated
+    after each chunk (Schur complement): W_r -= Delta [G_cc]^-1 G_cr, G <- G_rr - G_rc [G_cc]^-1 G_cr,
+    G = H^-1 at the start.  `quantiser(cols)` maps the chunk's column vectors (rows) to their
+    dequantised values.  With chunk = 1 the update is eq. optq_update with [H^-1]_ii."""
+    w = np.array(w, dtype=np.float64, copy=True)
+    d_in = w.shape[1]
+    g = np.linalg.inv(_damped(h, damp))
+    q = np.zeros_like(w)
+    for c0 in range(0, d_in, chunk):
+        c1 = min(c0 + chunk, d_in)
+        b = c1 - c0
+        q[:, c0:c1] = quantiser(w[:, c0:c1].T).T
+        delta = w[:, c0:c1] - q[:, c0:c1]
+        gcc, gcr, grr = g[:b, :b], g[:b, b:], g[b:, b:]
+        if c1 < d_in:
+            w[:, c1:] -= delta @ np.linalg.solve(gcc, gcr)
+            g = grr - gcr.T @ np.linalg.solve(gcc, gcr)
+    return q, w
 

@@ -521,3 +521,39 @@ def test_original_step_is_an_orthogonal_projection(rng):
         rho = rho - np.where(take_v[:, None], ref.apply_p(dlt, eps), dlt)
     assert (tr["choice"][:, -1] == -1).all()  # both rows reached the tolerance
     assert (np.sqrt((d["r"] ** 2).sum(axis=1)) < 1e-3).all()
+
+
+# ----------------------------------------------------------------------------- error compensation
+def _quantiser(eps, k):
+    return lambda cols: ref._quantise_columns(cols, eps, k, 0)[0]
+
+
+@pytest.mark.parametrize("chunk", [1, 4, 7, 24])
+def test_optq_cholesky_form_equals_hessian_downdate(chunk):
+    """The chunk update through the Cholesky factor of H^-1 equals the update written with the
+    inverse Hessian of the remaining columns and its Schur-complement downdate (with chunk = 1,
+    eq. optq_update with [H^-1]_ii column by column)."""
+    rng = np.random.default_rng(chunk)
+    dout, din, k = 40, 24, 6
+    w = rng.standard_normal((dout, din)) * 0.02
+    eps = ref.sign_mask(dout, 2)
+    h = ref.synthetic_hessian(din, 100, 5, outlier_cols=2, outlier_scale=8.0)
+    q, wf, _ = ref.optq_kashin(w, h, eps, k, chunk)
+    q2, wf2 = ref.optq_reference(w, h, chunk, _quantiser(eps, k))
+    np.testing.assert_allclose(q, q2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(wf, wf2, rtol=0, atol=1e-12)
+
+
+def test_optq_without_correlation_or_with_one_chunk_is_plain_quantisation(rng):
+    """H = I (uncorrelated inputs) leaves nothing to compensate, and so does a single chunk: both
+    give the per-column quantisation of W itself."""
+    dout, din, k = 32, 12, 5
+    w = rng.standard_normal((dout, din)) * 0.02
+    eps = ref.sign_mask(dout, 3)
+    plain = _quantiser(eps, k)(w.T).T
+    q, wf, _ = ref.optq_kashin(w, np.eye(din), eps, k, 4)
+    np.testing.assert_allclose(q, plain, atol=1e-14)
+    np.testing.assert_allclose(wf, w, atol=1e-14)
+    h = ref.synthetic_hessian(din, 60, 1)
+    q1, _, _ = ref.optq_kashin(w, h, eps, k, din)
+    np.testing.assert_allclose(q1, plain, atol=1e-14)
