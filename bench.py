@@ -16,6 +16,9 @@
   rows, for every matrix of the workload.
 --op schedule: one step = kashin_decompose_schedule (--schedule alternating | reverse | adaptive |
   original) over every matrix of the workload, 4k atomic steps, factors and residual written.
+--op optq: one step = the chunked error-compensated pipeline (paper_2609_11687_amd.optq) on one
+  matrix of the workload (--matrix, default q_proj): its columns quantised in chunks of --chunk
+  with the error carried through a synthetic Hessian (seeded activations with outlier channels).
 """
 from __future__ import annotations
 
@@ -38,6 +41,7 @@ METRIC_RECON = "weight rows reconstructed/s (w_hat = u_q + P v_q from 2+2-bit co
 METRIC_ROTATE = "weight rows rotated/s (R w, fp16 in, fp32 out); % of HBM roofline"
 METRIC_QUANT_H = "weight vectors rotated + decomposed + quantised/s (+H pipeline, N=4096, fixed iters)"
 METRIC_SCHED = "weight vectors decomposed/s with the {} step schedule (4k steps, both residual domains kept)"
+METRIC_OPTQ = "weight columns quantised/s with error compensation (chunks of {}, synthetic Hessian)"
 ROT_SEED = 1234  # seed of the rotation's sign vector
 PEAK_FP32_TFLOPS = 157.3   # MI355X published FP32 vector peak (256 CU x 2.4 GHz x 256 flop/clk)
 PEAK_HBM_GBPS = 8000.0     # MI355X published HBM3E bandwidth
@@ -210,8 +214,10 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama7b")
-    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h", "schedule"),
-                    default="quantize")
+    ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h", "schedule",
+                                     "optq"), default="quantize")
+    ap.add_argument("--matrix", default="q_proj", help="matrix of the workload (--op optq)")
+    ap.add_argument("--chunk", type=int, default=128, help="columns per compensation chunk (--op optq)")
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
@@ -305,6 +311,46 @@ def main() -> int:
                         spec.rows * (2 * nb + 32 + 4 * spec.n),
                         lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s),
                         kind="pmap"))
+    elif args.op == "optq":
+        from paper_2609_11687_amd import optq
+
+        names = [s_.name for s_ in wl.matrices]
+        chosen = list(range(len(names))) if args.matrix == "all" else [names.index(args.matrix)]
+        jobs = []
+        gemm = 0.0
+        g = torch.Generator(device=dev).manual_seed(0)
+        hess_by_din = {}
+        for idx in chosen:
+            spec = wl.matrices[idx]
+            log(f"generating {args.workload} {spec.name} {spec.rows}x{spec.n}")
+            w0_t = torch.from_numpy(synth.make_matrix(wl, 0, idx).T.copy()).to(dev).to(torch.float32).contiguous()
+            d_in, d_out = w0_t.shape
+            if d_in not in hess_by_din:  # one synthetic Hessian per input width
+                x = torch.randn((2 * d_in, d_in), dtype=torch.float32, device=dev, generator=g)
+                x[:, torch.randperm(d_in, generator=g, device=dev)[: max(1, d_in // 1000)]] *= 20.0
+                hess_by_din[d_in] = (x.t() @ x) / x.shape[0]
+                del x
+            plan = K.kashin_plan(d_out, synth.sign_seed(wl, 0, idx), wl.iters)
+            jobs.append((plan, w0_t, torch.empty_like(w0_t), hess_by_din[d_in], torch.cuda.Stream(dev)))
+            gemm += sum(2.0 * min(args.chunk, d_in - c0) * d_out * (d_in - min(c0 + args.chunk, d_in))
+                        for c0 in range(0, d_in, args.chunk))
+        keep.append(jobs)
+        nchunks = sum((j[1].shape[0] + args.chunk - 1) // args.chunk for j in jobs)
+
+        def run_optq(s):
+            # every matrix on its own stream, joined back into the timing stream
+            for plan, w0_t, w_t, hess, st in jobs:
+                st.wait_stream(s)
+                with torch.cuda.stream(st):
+                    w_t.copy_(w0_t)
+                optq.optq_quantize(plan, w_t, hess, args.chunk, lloyd_iters=args.lloyd, stream=st)
+            for *_, st in jobs:
+                s.wait_stream(st)
+
+        d_out = jobs[0][1].shape[1]
+        cols = sum(j[1].shape[0] for j in jobs)
+        flops = sum(j[1].shape[0] * counted_flops_per_vector(j[1].shape[1], wl.iters) for j in jobs) + gemm
+        launches.append(Launch(d_out, cols, flops, sum(j[1].numel() * 12 for j in jobs), run_optq, kind="optq"))
     else:
         g = torch.Generator(device=dev).manual_seed(0)
         for n in sorted({spec.n for spec in wl.matrices}):
@@ -323,14 +369,28 @@ def main() -> int:
 
     # dominant kernel: the N = 4096 launches (if present) of the op's main kernel, averaged over them
     main_kind = {"quantize": "quantize", "quantize_h": "quantize", "rotate": "rotate",
-                 "schedule": "schedule"}.get(args.op, "pmap")
+                 "schedule": "schedule", "optq": "optq"}.get(args.op, "pmap")
     dom_n = 4096 if 4096 in by_n else max(by_n, key=lambda n: by_n[n]["ms"])
     dom = [(l, ms) for l, ms in zip(launches, launch_ms) if l.n == dom_n and l.kind == main_kind]
     dom_s = sum(ms for _, ms in dom) / 1e3
     dom_flops = sum(l.flops for l, _ in dom)
     dom_bytes = sum(l.nbytes for l, _ in dom)
     layer = ", ".join(f"{s.name} {s.rows}x{s.n}" for s in wl.matrices) + f" x {wl.layers} layer(s)"
-    if main_kind == "schedule":
+    if main_kind == "optq":
+        achieved = dom_flops / dom_s / 1e12
+        roofline = {
+            "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
+            "kernel": f"optq pipeline ({len(jobs)} matrices, {nchunks} chunks: pair_greedy_kernel + pair_pmap_kernel "
+                      f"+ GEMM)",
+            "launches": len(dom), "counted_flops": dom_flops, "gemm_flops": gemm,
+        }
+        metric, unit = METRIC_OPTQ.format(args.chunk), "columns/s"
+        workload = (f"optq: {args.workload} " + ", ".join(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].n}"
+                                                           for i in chosen)
+                    + f" (each on its own stream), columns quantised in chunks of {args.chunk}, k={wl.iters}, "
+                    f"Hessian of 2 d_in seeded Gaussian activations with 0.1% outlier channels x20")
+    elif main_kind == "schedule":
         achieved = dom_flops / dom_s / 1e12
         roofline = {
             "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",

@@ -557,3 +557,54 @@ def test_schedule_replay_parity(n, schedule):
     np.testing.assert_allclose(r2.cpu().numpy(), rep["trace"]["r2"], rtol=1e-3, atol=1e-10 * (winf.max() ** 2) * n)
     if schedule == "original":
         assert (gch == -1).any()  # the tolerance stopped some rows
+
+
+# ----------------------------------------------------------------------------- error compensation
+def test_optq_pipeline_stepwise():
+    """The chunked error-compensated pipeline, checked chunk by chunk on the GPU's own state:
+    each chunk's codes against the oracle's decomposition of the same columns (replayed at
+    near-ties), its dequantised columns against the oracle's reconstruction of the GPU codes, and
+    the carried error against the oracle's U_cc^-1 U_cr applied to the GPU's Delta."""
+    from paper_2609_11687_amd import optq
+
+    d_out, d_in, chunk, k = 512, 192, 64, 20
+    rng = np.random.default_rng(21)
+    w = _rows(rng, d_in, d_out, "t4")  # W^T: one row per column of W
+    h = ref.synthetic_hessian(d_in, 400, 9, outlier_cols=4, outlier_scale=10.0)
+    seed = 41
+    eps = ref.sign_mask(d_out, seed)
+    plan = K.kashin_plan(d_out, seed, k)
+    w_t = pu.to_dev(w)
+    record = []
+    cu, cv, ce, q_t = optq.optq_quantize(plan, w_t, pu.to_dev(h), chunk, record=record)
+    torch.cuda.synchronize()
+    hd = h + 0.01 * np.mean(np.diag(h)) * np.eye(d_in)
+    u = np.linalg.cholesky(np.linalg.inv(hd)).T
+    scale = np.abs(w).max()
+    for snap in record:
+        c0, c1 = snap["c0"], snap["c1"]
+        wc = snap["w_chunk"].cpu().numpy().astype(np.float64)
+        qc = q_t[c0:c1].cpu().numpy().astype(np.float64)
+        # dequantised columns: the oracle's reconstruction of the GPU codes
+        qref = ref.reconstruct(pu.unpack(cu[c0:c1].cpu().numpy(), d_out), pu.unpack(cv[c0:c1].cpu().numpy(), d_out),
+                               ce[c0:c1].cpu().numpy().astype(np.float64), eps)
+        assert np.abs(qc - qref).max() <= 1e-5 * np.abs(qref).max()
+        # the decomposition of the chunk's columns, sampled rows replayed against the oracle
+        rows = [0, (c1 - c0) // 2, c1 - c0 - 1]
+        signs, _, u_tr, v_tr = pu.gpu_trace(plan, snap["w_chunk"], rows, k)
+        res = pu.replay_parity(wc[rows], eps, k, signs, u_tr, v_tr)
+        pu.assert_replay_ok(res, f"optq chunk {c0}")
+        if c0 > 0:
+            np.testing.assert_array_equal(wc, wc_rest[:c1 - c0])  # the chunk starts from the carried state
+        # the carried error
+        if c1 < d_in:
+            before = wc_rest if c0 > 0 else w.astype(np.float64)
+            before = before[c1 - c0:] if c0 > 0 else before[c1:]
+            m = np.linalg.solve(u[c0:c1, c0:c1], u[c0:c1, c1:])
+            expect = before - m.T @ (wc - qc)
+            got = snap["w_rest_after"].cpu().numpy().astype(np.float64)
+            err = np.abs(got - expect).max() / scale
+            _say(f"optq chunk {c0}:{c1}: carried-error mismatch {err:.2e}, du={res['du'].max():.2e}")
+            assert err <= 1e-5
+            wc_rest = got
+    del plan
