@@ -111,3 +111,15 @@ def test_rotate_validation_before_device():
     assert L.kashin_rotate(512, 0, 0, x, 1, 4, 512, x, 512, None) == K.KASHIN_E_INVALID
     assert "overlap" in L.kashin_last_error().decode()
     assert L.kashin_rotate(11008, 0, 1, x, 0, 0, 11008, y, 11008, None) == K.KASHIN_OK
+
+
+def test_schedule_validation_before_device():
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1234)
+    buf = ctypes.c_void_p(0x1000)
+    f = ctypes.c_float
+    # dead plan first, then the schedule arguments
+    assert L.kashin_decompose_schedule(fake, 0, f(0.0), buf, 0, 4, 512, buf, buf, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_trace_schedule(None, 2, f(0.0), buf, 0, 4, 512, buf, 1, buf, buf, buf, buf, buf, buf,
+                                   None) == K.KASHIN_E_INVALID
+    assert "plan" in L.kashin_last_error().decode()
