@@ -811,8 +811,9 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   // forward last pass (stride N/R), fused with the eps step and the inverse first pass
   float2 y[R];
   const float2* rb = lds + pad(t);
+  // the last pass reads and writes the same elements t + q N/R, which no other thread touches:
+  // no barrier between its read and its write
   if (act) sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
-  __syncthreads();
   launder_powers<C>(rr);
   if (act) {
     dft_pow2_tw<R, false>(y, [&](auto rv) { return last_tw<C, decltype(rv)::value>(rr); });  // y[q] = Y_{t + q NB}
