@@ -12,8 +12,8 @@
   of every matrix of the workload (quantized once, untimed).
 --op rotate: one step = the incoherence pre-rotation R w (kashin_rotate) of every matrix of the
   workload, fp16 rows in, fp32 rows out.
---op quantize_h: one step = the "+H" pipeline, R w followed by kashin_quantize of the rotated
-  rows, for every matrix of the workload.
+--op quantize_h: one step = the "+H" pipeline, kashin_quantize_rotated (R w formed in the load,
+  then quantised) over every matrix of the workload.
 --op schedule: one step = kashin_decompose_schedule (--schedule alternating | reverse | adaptive |
   original) over every matrix of the workload, 4k atomic steps, factors and residual written.
 --op optq: one step = the chunked error-compensated pipeline (paper_2609_11687_amd.optq) on one
@@ -277,7 +277,7 @@ def main() -> int:
                         lambda s, a=(plan, wd, uu, vv, rr_): K.kashin_decompose_schedule(
                             a[0], args.schedule, a[1], a[2], a[3], a[4], stream=s),
                         kind="schedule"))
-                elif args.op in ("rotate", "quantize_h"):
+                elif args.op == "rotate":
                     wr = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
                     keep.append((plan, wd, wr, cu, cv, ce))
                     p2 = spec.n & -spec.n
@@ -286,13 +286,13 @@ def main() -> int:
                         spec.rows * spec.n * (2 + 4),
                         lambda s, a=(spec.n, wd, wr): K.kashin_rotate(a[0], ROT_SEED, a[1], a[2], stream=s),
                         kind="rotate"))
-                    if args.op == "quantize_h":
-                        launches[-1].rows = 0  # counted once, on its quantize launch
-                        launches.append(Launch(
-                            spec.n, spec.rows, spec.rows * counted_flops_per_vector(spec.n, wl.iters),
-                            spec.rows * hbm_bytes_per_vector(spec.n, 4),
-                            lambda s, a=(plan, wr, cu, cv, ce): K.kashin_quantize(a[0], a[1], args.lloyd, a[2], a[3],
-                                                                                  a[4], s)))
+                elif args.op == "quantize_h":
+                    keep.append((plan, wd, cu, cv, ce))
+                    launches.append(Launch(
+                        spec.n, spec.rows, spec.rows * counted_flops_per_vector(spec.n, wl.iters),
+                        spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4),
+                        lambda s, a=(plan, wd, cu, cv, ce): K.kashin_quantize_rotated(
+                            a[0], ROT_SEED, a[1], args.lloyd, a[2], a[3], a[4], s)))
                 elif args.op == "quantize":
                     keep.append((plan, wd, cu, cv, ce))
                     launches.append(Launch(
@@ -404,12 +404,13 @@ def main() -> int:
                     f"{4 * wl.iters} atomic steps")
     elif main_kind == "quantize":
         achieved = dom_flops / dom_s / 1e12
+        kname = "pair_greedy_kernel[quantize" + (",lloyd" if args.lloyd > 0 else "") + \
+            (",rotated]" if args.op == "quantize_h" else "]")
         roofline = {
             "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_TFLOPS,
-            "traffic": measured_traffic(args.op, args.workload, "pair_greedy_kernel[quantize]",
-                                        [(l.n, (l.rows + 1) // 2) for l, _ in dom]),
-            "kernel": f"pair_greedy_kernel[quantize] N={dom_n}", "launches": len(dom),
+            "traffic": measured_traffic(args.op, args.workload, kname, [(l.n, (l.rows + 1) // 2) for l, _ in dom]),
+            "kernel": f"{kname} N={dom_n}", "launches": len(dom),
             "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
             "algorithmic_bytes_per_launch": dom_bytes / len(dom),
         }
@@ -419,8 +420,8 @@ def main() -> int:
                         f"lloyd={args.lloyd}, one row = one vector")
         else:
             metric, unit = METRIC_QUANT_H, "vectors/s"
-            workload = (f"{args.workload} +H: {layer}, {wl.matrices[0].dtype} rows rotated (R w, seed {ROT_SEED}) "
-                        f"to fp32, then quantised, k={wl.iters} blocks, lloyd={args.lloyd}")
+            workload = (f"{args.workload} +H: {layer}, {wl.matrices[0].dtype} rows rotated in the load (R w, seed "
+                        f"{ROT_SEED}) and quantised, k={wl.iters} blocks, lloyd={args.lloyd}")
     else:
         achieved = dom_bytes / dom_s / 1e9
         kname = f"rotate_kernel[b={dom_n // (dom_n & -dom_n)}]" if main_kind == "rotate" else "pair_pmap_kernel"

@@ -157,6 +157,20 @@ int kashin_trace_schedule(kashin_plan_t plan, int32_t schedule, float tol, const
 int kashin_rotate(int32_t n, uint64_t seed, int32_t inverse, const void* x, int32_t dtype, int64_t m,
                   int64_t ldx, float* y, int64_t ldy, void* stream);
 
+/* The "+H" pipeline with the rotation fused: kashin_quantize of R w (R as kashin_rotate with
+ * seed rot_seed; n = the plan's length), the rows rotated on the way in, so w is read once and the
+ * rotated rows are never written.  Codes and centres are those of R w; results equal
+ * kashin_rotate followed by kashin_quantize of its fp32 output bit for bit. */
+int kashin_quantize_rotated(kashin_plan_t plan, uint64_t rot_seed, const void* w, int32_t dtype, int64_t m,
+                            int64_t ldw, int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers,
+                            void* stream);
+
+/* Load-time reconstitution of a rotated quantisation: w_hat = R^T (u_q + P v_q), equal to
+ * kashin_reconstruct followed by the inverse kashin_rotate bit for bit.  Layouts as
+ * kashin_reconstruct. */
+int kashin_reconstruct_rotated(kashin_plan_t plan, uint64_t rot_seed, const uint8_t* codes_u, const uint8_t* codes_v,
+                               const float* centers, int64_t m, float* w_hat, int64_t ldw, void* stream);
+
 /* Test hook: replay record of Alg. 2 for selected rows.  For each of the `nrows` row
  * indices in `rows` (device int64, each in [0, m)), the row is decomposed exactly as
  * kashin_decompose does (paired with the same neighbour) and the kernel writes

@@ -146,6 +146,13 @@ kashin::KArgs base_args(const kashin_plan_s* p, int mode) {
   return a;
 }
 
+// the rotation fused into a pair kernel: seed and 1 / sqrt(2^a), n = 2^a b (as kashin_rotate)
+void set_rotation(kashin::KArgs* a, int n, uint64_t seed) {
+  a->rot = 1;
+  a->rot_seed = seed;
+  a->rot_scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n & -n)));
+}
+
 int launch(const kashin_plan_s* p, const kashin::KArgs& a, int64_t grid, void* stream) {
   const hipError_t e = kashin::launch_pair(p->n, a, grid, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -370,6 +377,47 @@ int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void
   a.ldw = plan->n;
   a.y = y;
   a.ldy = plan->n;
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_quantize_rotated(kashin_plan_t plan, uint64_t rot_seed, const void* w, int32_t dtype, int64_t m,
+                            int64_t ldw, int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers,
+                            void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
+  if (m == 0) return ok();
+  if (!w || !codes_u || !codes_v || !centers) return fail(KASHIN_E_INVALID, "w, codes and centers must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_QUANTIZE);
+  a.w = w;
+  a.dtype = dtype;
+  a.m = m;
+  a.ldw = ldw;
+  a.lloyd = lloyd_iters;
+  a.codes_u = codes_u;
+  a.codes_v = codes_v;
+  a.centers = centers;
+  set_rotation(&a, plan->n, rot_seed);
+  return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_reconstruct_rotated(kashin_plan_t plan, uint64_t rot_seed, const uint8_t* codes_u, const uint8_t* codes_v,
+                               const float* centers, int64_t m, float* w_hat, int64_t ldw, void* stream) {
+  int st = check_common(plan, m);
+  if (st) return st;
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (m == 0) return ok();
+  if (!codes_u || !codes_v || !centers || !w_hat) return fail(KASHIN_E_INVALID, "codes, centers and w_hat must be non-null");
+  kashin::KArgs a = base_args(plan, kashin::MODE_RECON);
+  a.w = codes_u;
+  a.in_codes_v = codes_v;
+  a.in_centers = centers;
+  a.m = m;
+  a.y = w_hat;
+  a.ldy = ldw;
+  set_rotation(&a, plan->n, rot_seed);
   return launch(plan, a, (m + 1) / 2, stream);
 }
 

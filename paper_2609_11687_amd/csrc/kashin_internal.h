@@ -58,6 +58,10 @@ struct KArgs {
   float tol;
   int8_t* tr_choice;
   float* tr_r2;
+  // incoherence rotation fused into the load (quantize, decompose, trace) or the store (recon)
+  int32_t rot;
+  float rot_scale;  // 1 / sqrt(2^a), n = 2^a b
+  uint64_t rot_seed;
 };
 
 struct ClusterArgs {

@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "kashin_internal.h"
+#include "kashin_rot_impl.h"
 #include "kashin_tables.h"
 
 namespace kashin {
@@ -935,6 +936,39 @@ __device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restr
   }
 }
 
+// R w for both rows of the pair (the rotation fused into the load): the rows are staged in the
+// LDS buffer in row order as float2 (row a in .x, row b in .y), signed, mixed by C_b and the
+// Hadamard factor, and read back in the register layout times 1 / sqrt(2^a) -- the same
+// operations in the same order as the standalone rotation kernel.  Uses the whole buffer.
+template <class C, class IT>
+__device__ __forceinline__ void load_pair_rot_t(float2 (&z)[C::E], const IT* __restrict__ w, int64_t ldw, int64_t ra,
+                                                int64_t rb, uint64_t seed, float scale, float2* lds) {
+  constexpr int N = C::N;
+  constexpr int B = rot_odd_part(N);
+  const int tid = threadIdx.x;
+  const IT* pa = w + ra * ldw;
+  const IT* pb = w + (rb >= 0 ? rb : ra) * ldw;
+  __syncthreads();  // the buffer may still be read by the last pass of a transform
+  for (int i = tid; i < N; i += C::T) {
+    const float s = rot_sign(seed, i);
+    lds[i] = make_float2(to_f32(pa[i]) * s, rb >= 0 ? to_f32(pb[i]) * s : 0.f);
+  }
+  __syncthreads();
+  rot_odd_factor<B, false, C::T>(lds, N, tid);
+  rot_hadamard<B, C::T>(lds, N, tid);
+#pragma unroll
+  for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
+  for_each_elem<C>([&](int e, int i) { z[e] = rv_scale(lds[i], scale); });
+  __syncthreads();  // read before the first pass overwrites the buffer
+}
+
+template <class C>
+__device__ __forceinline__ void load_pair_rot(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
+                                              int64_t rb, uint64_t seed, float scale, float2* lds) {
+  if (dtype == 1) load_pair_rot_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, seed, scale, lds);
+  else load_pair_rot_t<C>(z, static_cast<const float*>(w), ldw, ra, rb, seed, scale, lds);
+}
+
 template <class C>
 __device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
                                           int64_t rb, int tid = static_cast<int>(threadIdx.x)) {
@@ -1125,8 +1159,9 @@ __device__ __forceinline__ void store_centers(float* centers, int f, const float
 // first factor is recovered exactly as u = w - P(z + vhat), since w = u + P vhat + P z.
 // QUANT selects the fused quantizer instance (MODE_QUANTIZE), the other one serves
 // MODE_DECOMPOSE and MODE_TRACE; LLOYD (QUANT only) the instance with k-means refinement
-// after the closed form.  Each instance carries only the registers of its own epilogue.
-template <class C, bool LLOYD, bool QUANT>
+// after the closed form; ROT (QUANT only) the instance with the rotation fused into the loads.
+// Each instance carries only the code and registers of its own variant.
+template <class C, bool LLOYD, bool QUANT, bool ROT>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_greedy_kernel(
     KArgs a, int64_t item0) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
@@ -1154,7 +1189,8 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   };
 
   float2 z[C::E], vh[C::E];
-  load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
+  if constexpr (ROT) load_pair_rot<C>(z, a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds);
+  else load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
   float2 scale, unscale;
   bool bad_a, bad_b;
   normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
@@ -1235,7 +1271,17 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
 #pragma unroll
   for (int e = 0; e < C::E; ++e) z[e] = cadd(z[e], vh[e]);
   applyP(z);
-  sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
+  if constexpr (ROT) {
+    float2 t[C::E];
+    load_pair_rot<C>(t, a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds);
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) {
+      z[e].x = bad_a ? 0.f : fmaf(t[e].x, scale.x, -z[e].x);
+      z[e].y = bad_b ? 0.f : fmaf(t[e].y, scale.y, -z[e].y);
+    }
+  } else {
+    sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
+  }
   float2(&u)[C::E] = z;
 
   if constexpr (QUANT) {
@@ -1312,7 +1358,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
 // buffer, in row order, so codes are read one byte per four elements and w_hat is written in
 // contiguous 16-byte vectors; y = P x loads and stores in the register layout directly
 // (measured faster for it than staging).
-template <class C>
+template <class C, bool ROT>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_pmap_kernel(
     KArgs a, int64_t item0, int64_t nitems) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
@@ -1378,6 +1424,45 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
         if (rb >= 0) a.y[rb * a.ldy + i] = bad_b ? qnan : z[e].y * unscale.y;
       }, tid);
       __syncthreads();  // the last pass read the buffer the next item's first pass writes
+      continue;
+    }
+    if constexpr (ROT) {
+      // w_hat = R^T (P v_q + u_q): both rows in row order as float2, u_q added, then the
+      // Hadamard factor, C_b^T, the scale and the signs, as the standalone inverse rotation
+      constexpr int B = rot_odd_part(N);
+      __syncthreads();  // the last pass read the buffer
+      for_each_elem<C>([&](int e, int i) {
+        lds[i] = make_float2(bad_a ? qnan : z[e].x * unscale.x, bad_b ? qnan : z[e].y * unscale.y);
+      }, tid);
+      __syncthreads();
+      const uint8_t* cua = static_cast<const uint8_t*>(a.w) + ra * NBY;
+      const uint8_t* cub = static_cast<const uint8_t*>(a.w) + (rb >= 0 ? rb : ra) * NBY;
+      const float* cea = a.in_centers + ra * 8;
+      const float* ceb = a.in_centers + (rb >= 0 ? rb : ra) * 8;
+      const float ua[4] = {cea[0], cea[1], cea[2], cea[3]};
+      const float ub[4] = {ceb[0], ceb[1], ceb[2], ceb[3]};
+      for (int q = tid; q < NBY; q += C::T) {
+        const uint32_t ba = cua[q], bb = cub[q];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          float2 v = lds[4 * q + k];
+          v.x += pick4(ua, (ba >> (2 * k)) & 3);
+          v.y += pick4(ub, (bb >> (2 * k)) & 3);
+          lds[4 * q + k] = v;
+        }
+      }
+      __syncthreads();
+      rot_hadamard<B, C::T>(lds, N, tid);
+      rot_odd_factor<B, true, C::T>(lds, N, tid);
+      float* ya = a.y + ra * a.ldy;
+      float* yb = a.y + (rb >= 0 ? rb : ra) * a.ldy;
+      for (int i = tid; i < N; i += C::T) {
+        const float s = rot_sign(a.rot_seed, i);
+        const float2 v = lds[i];
+        ya[i] = v.x * a.rot_scale * s;
+        if (rb >= 0) yb[i] = v.y * a.rot_scale * s;
+      }
+      __syncthreads();  // read before the next item's first pass writes the buffer
       continue;
     }
     __syncthreads();  // the last pass read the buffer the outputs are staged in
@@ -1608,21 +1693,21 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
   constexpr int64_t kMaxGrid = int64_t(1) << 30;
   for (int64_t i0 = 0; i0 < grid; i0 += kMaxGrid) {
     const int64_t g = (grid - i0 < kMaxGrid) ? grid - i0 : kMaxGrid;
-    if (a.mode == MODE_QUANTIZE && a.lloyd > 0) {
-      hipLaunchKernelGGL((pair_greedy_kernel<C, true, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
-                         i0);
-    } else if (a.mode == MODE_QUANTIZE) {
-      hipLaunchKernelGGL((pair_greedy_kernel<C, false, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
-                         i0);
+    const dim3 gd(static_cast<unsigned>(g)), bd(C::T);
+    if (a.mode == MODE_QUANTIZE) {
+      if (a.lloyd > 0 && a.rot) hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, true>), gd, bd, 0, s, a, i0);
+      else if (a.lloyd > 0) hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, false>), gd, bd, 0, s, a, i0);
+      else if (a.rot) hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, true>), gd, bd, 0, s, a, i0);
+      else hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, false>), gd, bd, 0, s, a, i0);
     } else if (a.mode <= MODE_TRACE) {
-      hipLaunchKernelGGL((pair_greedy_kernel<C, false, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a,
-                         i0);
+      hipLaunchKernelGGL((pair_greedy_kernel<C, false, false, false>), gd, bd, 0, s, a, i0);
     } else if (a.mode == MODE_SCHEDULE) {
       hipLaunchKernelGGL(pair_schedule_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
     } else {
       constexpr int64_t kPmapGrid = 2048;  // resident workgroups of the whole chip, a few times over
       const int64_t pg = g < kPmapGrid ? g : kPmapGrid;
-      hipLaunchKernelGGL(pair_pmap_kernel<C>, dim3(static_cast<unsigned>(pg)), dim3(C::T), 0, s, a, i0, g);
+      if (a.rot) hipLaunchKernelGGL((pair_pmap_kernel<C, true>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      else hipLaunchKernelGGL((pair_pmap_kernel<C, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

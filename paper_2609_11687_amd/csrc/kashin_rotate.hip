@@ -4,10 +4,9 @@
 // splitmix64 output of the seed is set (the generator of the plan's sign mask).
 //
 // One workgroup per row, the row held in LDS (n <= 16384 floats).  Element n = i b + j; the odd
-// factor mixes the b contiguous entries of each segment i (one thread per segment, in place, the
-// constants compile-time), the Hadamard factor mixes entries with equal j across segments
-// (radix-2 stages in place, one barrier per stage).  The two factors commute, so R applies
-// signs, C_b, H and R^T applies H, C_b^T, signs.
+// factor mixes the b contiguous entries of each segment i, the Hadamard factor mixes entries with
+// equal j across segments (kashin_rot_impl.h).  The two factors commute, so R applies signs,
+// C_b, H and R^T applies H, C_b^T, signs.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -15,7 +14,7 @@
 #include <cstdint>
 
 #include "kashin_internal.h"
-#include "kashin_tables.h"
+#include "kashin_rot_impl.h"
 
 namespace kashin {
 namespace {
@@ -23,58 +22,8 @@ namespace {
 constexpr int kRotThreads = 256;
 constexpr int kRotMaxN = 16384;
 
-__device__ __forceinline__ float rot_sign(uint64_t seed, int i) {
-  uint64_t z = seed + static_cast<uint64_t>(i + 1) * 0x9E3779B97F4A7C15ull;
-  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-  z ^= z >> 31;
-  return (z >> 63) ? -1.f : 1.f;
-}
-
 __device__ __forceinline__ float load_f32(const float* p) { return *p; }
 __device__ __forceinline__ float load_f32(const __half* p) { return __half2float(*p); }
-
-// segment i of length B: v <- C_B v (or C_B^T v), in place
-template <int B, bool TRANS>
-__device__ __forceinline__ void odd_segment(float* seg) {
-  float in[B];
-#pragma unroll
-  for (int j = 0; j < B; ++j) in[j] = seg[j];
-#pragma unroll
-  for (int k = 0; k < B; ++k) {
-    float acc = 0.f;
-#pragma unroll
-    for (int j = 0; j < B; ++j) acc = fmaf(TRANS ? DctTab<B>::m[j * B + k] : DctTab<B>::m[k * B + j], in[j], acc);
-    seg[k] = acc;
-  }
-}
-
-template <int B, bool TRANS>
-__device__ __forceinline__ void odd_factor(float* buf, int n) {
-  if constexpr (B > 1) {
-    for (int i = threadIdx.x; i < n / B; i += kRotThreads) odd_segment<B, TRANS>(buf + i * B);
-    __syncthreads();
-  }
-}
-
-// unnormalised Walsh-Hadamard transform over the 2^a segments (stride B), in place
-template <int B>
-__device__ __forceinline__ void hadamard_factor(float* buf, int n) {
-  const int p2 = n / B;
-  for (int lh = 0; (1 << lh) < p2; ++lh) {
-    const int h = 1 << lh;
-    for (int t = threadIdx.x; t < n / 2; t += kRotThreads) {
-      const int q = t / B, j = t - q * B;  // butterfly q of the stage, column j
-      const int i0 = ((q >> lh) << (lh + 1)) | (q & (h - 1));
-      float* p0 = buf + i0 * B + j;
-      float* p1 = p0 + h * B;
-      const float a = *p0, b = *p1;
-      *p0 = a + b;
-      *p1 = a - b;
-    }
-    __syncthreads();
-  }
-}
 
 template <int B, bool INV, class IT>
 __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t seed, float scale, const IT* x,
@@ -87,12 +36,13 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t see
     buf[i] = INV ? v : v * rot_sign(seed, i);
   }
   __syncthreads();
+  const int tid = threadIdx.x;
   if constexpr (!INV) {
-    odd_factor<B, false>(buf, n);
-    hadamard_factor<B>(buf, n);
+    rot_odd_factor<B, false, kRotThreads>(buf, n, tid);
+    rot_hadamard<B, kRotThreads>(buf, n, tid);
   } else {
-    hadamard_factor<B>(buf, n);
-    odd_factor<B, true>(buf, n);
+    rot_hadamard<B, kRotThreads>(buf, n, tid);
+    rot_odd_factor<B, true, kRotThreads>(buf, n, tid);
   }
   float* yr = y + row * ldy;
   for (int i = threadIdx.x; i < n; i += kRotThreads) {

@@ -25,7 +25,8 @@ EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
     "kashin_quantize", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
-    "kashin_trace_schedule", "kashin_status_string", "kashin_last_error",
+    "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_status_string",
+    "kashin_last_error",
 )
 SCHEDULES = {"alternating": 0, "reverse": 1, "adaptive": 2, "original": 3}
 
@@ -60,6 +61,8 @@ def lib() -> ctypes.CDLL:
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
         "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
+        "kashin_quantize_rotated": [vp, u64, vp, i32, i64, i64, i32, vp, vp, vp, vp],
+        "kashin_reconstruct_rotated": [vp, u64, vp, vp, vp, i64, vp, i64, vp],
         "kashin_decompose_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, vp, vp, vp],
         "kashin_trace_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp],
         "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
@@ -210,6 +213,18 @@ def kashin_trace_schedule(plan, schedule, w, rows, sign_trace, c_trace, choice_t
     _check(lib().kashin_trace_schedule(plan.handle, SCHEDULES[schedule], tol, _ptr(w), _dtype_code(w), m, ldw,
                                        _ptr(rows), rows.numel(), _ptr(sign_trace), _ptr(c_trace), _ptr(choice_trace),
                                        _ptr(r2_trace), _ptr(u), _ptr(vhat), _stream(stream)))
+
+
+def kashin_quantize_rotated(plan, rot_seed, w, lloyd_iters, codes_u, codes_v, centers, stream=None):
+    m, ldw = _rows(w)
+    _check(lib().kashin_quantize_rotated(plan.handle, rot_seed, _ptr(w), _dtype_code(w), m, ldw, lloyd_iters,
+                                         _ptr(codes_u), _ptr(codes_v), _ptr(centers), _stream(stream)))
+
+
+def kashin_reconstruct_rotated(plan, rot_seed, codes_u, codes_v, centers, w_hat, stream=None):
+    m, ldw = _rows(w_hat)
+    _check(lib().kashin_reconstruct_rotated(plan.handle, rot_seed, _ptr(codes_u), _ptr(codes_v), _ptr(centers), m,
+                                            _ptr(w_hat), ldw, _stream(stream)))
 
 
 def kashin_rotate(n, seed, x, y, inverse=False, stream=None):

@@ -34,9 +34,11 @@ def _short(name: str) -> tuple[str, int]:
     rot = re.search(r"rotate_kernel<(\d+), (true|false)", name)  # rotate_kernel<odd factor, inverse, input type>
     if rot:
         base += f"[b={rot.group(1)}" + (",inverse]" if rot.group(2) == "true" else "]")
-    flags = re.search(r">, (true|false), (true|false)>", name)  # pair_greedy_kernel<Cfg, LLOYD, QUANT>
+    # pair_greedy_kernel<Cfg, LLOYD, QUANT, ROT>
+    flags = re.search(r">, (true|false), (true|false), (true|false)>", name)
     if flags:
-        base += ("[quantize" + (",lloyd" if flags.group(1) == "true" else "") + "]"
+        base += ("[quantize" + (",lloyd" if flags.group(1) == "true" else "") +
+                 (",rotated" if flags.group(3) == "true" else "") + "]"
                  if flags.group(2) == "true" else "[decompose]")
     return base, int(c.group(1)) if c else 0
 

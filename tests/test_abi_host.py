@@ -123,3 +123,21 @@ def test_schedule_validation_before_device():
     assert L.kashin_trace_schedule(None, 2, f(0.0), buf, 0, 4, 512, buf, 1, buf, buf, buf, buf, buf, buf,
                                    None) == K.KASHIN_E_INVALID
     assert "plan" in L.kashin_last_error().decode()
+
+
+def test_rotated_entry_points_reject_dead_plan():
+    """The fused-rotation entry points validate the plan like their unrotated forms (the
+    rotation itself needs no argument beyond the seed: every plan length has odd part 1, 3 or 43)."""
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1234)
+    buf = ctypes.c_void_p(0x1000)
+    assert L.kashin_quantize_rotated(None, 7, buf, 0, 4, 512, 0, buf, buf, buf, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_rotated(fake, 7, buf, 0, 4, 512, 0, buf, buf, buf, None) == K.KASHIN_E_INVALID
+    assert L.kashin_reconstruct_rotated(fake, 7, buf, buf, buf, 4, buf, 512, None) == K.KASHIN_E_INVALID
+    assert "plan" in L.kashin_last_error().decode()
+
+
+@pytest.mark.parametrize("n", [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 8192, 11008, 16384])
+def test_every_plan_length_is_rotatable(n):
+    assert K.kashin_supported_n(n)
+    assert n // (n & -n) in (1, 3, 43)

@@ -608,3 +608,32 @@ def test_optq_pipeline_stepwise():
             assert err <= 1e-5
             wc_rest = got
     del plan
+
+
+@pytest.mark.parametrize("n", [172, 512, 768, 4096, 11008])
+def test_fused_rotation_equals_separate_passes(n):
+    """kashin_quantize_rotated (rotation fused into the load) gives the codes and centres of
+    kashin_rotate followed by kashin_quantize, bit for bit, for fp16 and fp32 rows (odd row count:
+    an unpaired last row); kashin_reconstruct_rotated equals kashin_reconstruct followed by the
+    inverse rotation bit for bit."""
+    rng = np.random.default_rng(5 * n)
+    m, k, rot_seed = 5, 8, 99 + n
+    plan = K.kashin_plan(n, 7 + n, k)
+    for dt in (torch.float32, torch.float16):
+        wd = pu.to_dev(_rows(rng, m, n, "outlier")).to(dt)
+        wr = torch.empty((m, n), dtype=torch.float32, device="cuda")
+        K.kashin_rotate(n, rot_seed, wd, wr)
+        cu, cv, ce = K.quantize_alloc(plan, wr, 0)
+        fu, fv, fc = torch.empty_like(cu), torch.empty_like(cv), torch.empty_like(ce)
+        K.kashin_quantize_rotated(plan, rot_seed, wd, 0, fu, fv, fc)
+        wh = torch.empty((m, n), dtype=torch.float32, device="cuda")
+        K.kashin_reconstruct(plan, cu, cv, ce, wh)
+        K.kashin_rotate(n, rot_seed, wh, wh, inverse=True)
+        fh = torch.empty_like(wh)
+        K.kashin_reconstruct_rotated(plan, rot_seed, cu, cv, ce, fh)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(fu.cpu().numpy(), cu.cpu().numpy())
+        np.testing.assert_array_equal(fv.cpu().numpy(), cv.cpu().numpy())
+        np.testing.assert_array_equal(fc.cpu().numpy(), ce.cpu().numpy())
+        np.testing.assert_array_equal(fh.cpu().numpy(), wh.cpu().numpy())
+    _say(f"fused rotation N={n}: equal to the separate passes")
