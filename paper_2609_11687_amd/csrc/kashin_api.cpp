@@ -67,8 +67,6 @@ void make_signs(int32_t n, uint64_t seed, int8_t* out) {
   }
 }
 
-int pad_slot(int i) { return i + (i >> 4); }  // LDS slot of element i (kernel layout)
-
 // Tables of the pair kernel for length n (layout shared with kashin_pair_impl.h):
 //  tw:  one table per Stockham pass with stride NS > 1 -- forward passes 1..np-1, then
 //       inverse passes 1..np-1 (radices in reverse order) -- entry [jm][r] =
@@ -80,6 +78,7 @@ int pad_slot(int i) { return i + (i >> 4); }  // LDS slot of element i (kernel l
 void build_tables(int n, const int8_t* eps, std::vector<float2>* tw, std::vector<float4>* mid) {
   kashin::PlanShape sh;
   kashin::plan_shape(n, &sh);
+  const bool wide = kashin::uniform_resident(n, sh.threads, sh.np, sh.rad);
   const double pi = 3.14159265358979323846;
   auto add_table = [&](int R, int NS) {
     for (int jm = 0; jm < NS; ++jm)
@@ -119,7 +118,7 @@ void build_tables(int n, const int8_t* eps, std::vector<float2>* tw, std::vector
         fy = float(ek * std::sin(ang) / n);
         src = partner;
       }
-      const int addr = pad_slot(src) * int(sizeof(float2));
+      const int addr = kashin::pad_slot(n, wide, src) * int(sizeof(float2));
       float faddr;
       std::memcpy(&faddr, &addr, sizeof(faddr));
       (*mid)[j * R + r] = make_float4(fx, fy, faddr, 0.f);

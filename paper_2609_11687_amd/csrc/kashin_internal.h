@@ -86,6 +86,33 @@ struct PlanShape {
 };
 bool plan_shape(int n, PlanShape* out);
 
+// Whether the pair kernel's transform of length n (threads per workgroup, forward radices
+// rad[0..np)) has a single radix r = rad[0] <= 16, a power of two, with one butterfly of every
+// pass per thread (threads = n / r, a multiple of 32): such transforms stay resident in LDS and
+// take the wide padding below.
+__host__ __device__ constexpr bool uniform_resident(int n, int threads, int np, const int* rad) {
+  if (np < 2 || rad[0] > 16 || (rad[0] & (rad[0] - 1)) != 0 || threads != n / rad[0] || (n / rad[0]) % 32 != 0)
+    return false;
+  for (int p = 1; p < np; ++p)
+    if (rad[p] != rad[0]) return false;
+  return true;
+}
+
+// LDS layout of the pair kernel's transform buffer: element i of a length-n vector lives at
+// float2 slot i + pad_width(w) * (i >> pad_shift(n, w)), w = uniform_resident(...).  gfx950
+// resolves bank conflicts of an 8-byte LDS read per 32 lanes over 64 four-byte banks, of an
+// 8-byte write per 16 lanes over 32 banks and of a 16-byte write per 8 lanes over 32 banks.
+// Contiguous reads therefore want no gap inside an aligned run of 32 elements and stride-16
+// writes a spare slot per 16 elements.  Uniform resident transforms take two spare slots per
+// 32 elements (their first pass writes its stride-16 outputs as 16-byte pairs from a lane
+// order that puts one parity of butterflies in each eight lanes); other lengths that are
+// multiples of 512 one per 32, the rest (pass strides of 16 times an odd number) one per 16.
+__host__ __device__ constexpr int pad_shift(int n, bool wide) { return (wide || n % 512 == 0) ? 5 : 4; }
+__host__ __device__ constexpr int pad_width(bool wide) { return wide ? 2 : 1; }
+__host__ __device__ constexpr int pad_slot(int n, bool wide, int i) {
+  return i + pad_width(wide) * (i >> pad_shift(n, wide));
+}
+
 bool supported_n(int n);
 // Launch the pair kernel for vector length n; grid = number of work items (pairs or listed rows).
 hipError_t launch_pair(int n, const KArgs& a, int64_t grid, hipStream_t stream);

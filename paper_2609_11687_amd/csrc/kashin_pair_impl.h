@@ -242,7 +242,11 @@ struct Cfg {
   static constexpr int B0 = (NB0 + T - 1) / T;
   static constexpr int E = B0 * R0;
   static constexpr int NW = (T + 63) / 64;
-  static constexpr int LDS = N + (N >> 4) + 4;
+  static constexpr bool WIDE = uniform_resident(N_, T_, NP, rad);
+  static constexpr int PS = pad_shift(N_, WIDE);  // LDS padding: PW spare slots per PG elements
+  static constexpr int PW = pad_width(WIDE);
+  static constexpr int PG = 1 << PS;
+  static constexpr int LDS = N + PW * (N >> PS) + 4;
 };
 
 template <class C>
@@ -258,9 +262,34 @@ constexpr int ns_inv(int p) {
   return s;
 }
 
-// LDS layout: element k of the length-N complex vector lives at float2 slot pad(k) (one
-// spare slot per 16 elements, so stride-16 accesses of a Stockham pass spread over banks).
-__host__ __device__ constexpr int pad(int i) { return i + (i >> 4); }
+// LDS layout: element k of the length-N complex vector lives at float2 slot pad<C>(k) (C::PW
+// spare slots per C::PG elements, so that both contiguous and stride-16 accesses of a Stockham
+// pass spread over the banks).  pad<C>(x + y) = pad<C>(x) + pad<C>(y) whenever x mod PG +
+// y mod PG < PG: a base slot plus compile-time offsets addresses a butterfly's elements.
+template <class C>
+__host__ __device__ constexpr int pad(int i) { return i + C::PW * (i >> C::PS); }
+// Whether a Stockham write (element q of butterfly j to b + q S, b = (j / S) S R + j mod S,
+// q < R) can address slots as pad(b) + pad(q S): S a multiple of PG, or S dividing PG with
+// S R a multiple or a divisor of PG (then b mod PG + q S mod PG < PG for every q).
+template <class C>
+constexpr bool pad_offsets_ok(int S, int R) {
+  return S % C::PG == 0 || (C::PG % S == 0 && ((S * R) % C::PG == 0 || C::PG % (S * R) == 0));
+}
+
+// Butterfly index of thread l.  With two spare slots per 32 elements the resident transform
+// gives the butterflies of each 16-lane group to its lanes in the order 0, 2, .., 14, 1, 3, ..,
+// 15: the first pass then writes its outputs 16t + q, q < 16, as 16-byte pairs, and the eight
+// lanes of such a write (butterflies of one parity) cover 32 distinct banks.  Every other
+// access of the transform touches the same 16- and 32-lane index sets as in lane order.
+template <class C>
+constexpr bool lane_perm() {
+  return C::WIDE;
+}
+template <class C>
+__device__ __forceinline__ int bfly(int l) {
+  if constexpr (lane_perm<C>()) return (l & ~15) | (2 * (l & 7)) | ((l >> 3) & 1);
+  else return l;
+}
 
 // Opaque copy of the thread index: without it every twiddle load and LDS address of every
 // pass is proven invariant across the block loop, hoisted out of it, and kept live in
@@ -406,7 +435,7 @@ __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__
   constexpr bool FULL = (NB % T) == 0;
   static_assert(SRC != SRC_REGS || (R == C::R0 && NS == 1), "register source must be the first pass");
   static_assert(DST != DST_REGS || (R == C::R0 && NS == N / C::R0), "register target must be the last pass");
-  const int tid = opaque(static_cast<int>(threadIdx.x));
+  const int tid = opaque(bfly<C>(threadIdx.x));
   float2 a[BP][R];
   sfor<0, BP>([&](auto iv) {
     constexpr int i = decltype(iv)::value;
@@ -424,11 +453,11 @@ __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__
           a[i][r] = make_float2(f.x * v.x - f.y * v.y, f.x * v.y + f.y * v.x);
           if constexpr (R > 16 && r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
         });
-      } else if constexpr (NB % 16 == 0) {
-        const float2* base = lds + pad(j);
-        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = base[decltype(rv)::value * pad(NB)]; });
+      } else if constexpr (NB % C::PG == 0) {
+        const float2* base = lds + pad<C>(j);
+        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = base[decltype(rv)::value * pad<C>(NB)]; });
       } else {
-        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = lds[pad(j + decltype(rv)::value * NB)]; });
+        sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = lds[pad<C>(j + decltype(rv)::value * NB)]; });
       }
     }
   });
@@ -467,20 +496,17 @@ __device__ __forceinline__ void fft_pass(float2 (&z)[C::E], float2* __restrict__
             if constexpr (!INV) return make_float2(v.x * t.x - v.y * t.y, v.x * t.y + v.y * t.x);
             else return make_float2(v.x * t.x + v.y * t.y, v.y * t.x - v.x * t.y);
           };
-          if constexpr (NS % 16 == 0) {
-            float2* base = lds + pad(idx0);
-            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { base[q * pad(NS)] = v; });
+          if constexpr (pad_offsets_ok<C>(NS, R)) {
+            float2* base = lds + pad<C>(idx0);
+            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { base[pad<C>(q * NS)] = v; });
           } else {
-            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+            dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { lds[pad<C>(idx0 + q * NS)] = v; });
           }
-        } else if constexpr (NS % 16 == 0) {
-          float2* base = lds + pad(idx0);
-          dft<R, INV>(a[i], [&](int q, float2 v) { base[q * pad(NS)] = v; });
-        } else if constexpr (NS == 1 && 16 % R == 0) {
-          float2* base = lds + pad(idx0);
-          dft<R, INV>(a[i], [&](int q, float2 v) { base[q] = v; });
+        } else if constexpr (pad_offsets_ok<C>(NS, R)) {
+          float2* base = lds + pad<C>(idx0);
+          dft<R, INV>(a[i], [&](int q, float2 v) { base[pad<C>(q * NS)] = v; });
         } else {
-          dft<R, INV>(a[i], [&](int q, float2 v) { lds[pad(idx0 + q * NS)] = v; });
+          dft<R, INV>(a[i], [&](int q, float2 v) { lds[pad<C>(idx0 + q * NS)] = v; });
         }
       } else {
         dft<R, INV>(a[i], [&](int q, float2 v) { z[i * R + q] = v; });
@@ -539,7 +565,7 @@ constexpr bool has_split_pass() {
 template <class C>
 constexpr bool resident_ok() {
   constexpr int R0 = C::R0;
-  if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % 16 == 0))
+  if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % C::PG == 0))
     return false;
   if (has_split_pass<C>()) return C::T >= C::N / R0;
   for (int p = 0; p < C::NP; ++p)
@@ -595,7 +621,7 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
                                               const float4* __restrict__ mid) {
   constexpr int R = C::R0;
   constexpr int NB = C::N / R;
-  const int t = threadIdx.x;
+  const int t = bfly<C>(threadIdx.x);
   const int tl = (C::T == NB || t < NB) ? t : 0;  // threads past the last butterfly load row 0 (unused)
   const float4* t4 = reinterpret_cast<const float4*>(tw + tw_offset<C, false>(C::NP - 1) + tl * R);
   sfor<0, R / 2>([&](auto hv) {
@@ -612,9 +638,10 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
     const float4 m = mid[tl * R + decltype(rv)::value];
     rr.f[decltype(rv)::value] = make_float2(m.x, m.y);
   });
-  // inner-pass tables, transposed to [r][jm] so that the lanes of a wave (consecutive jm)
-  // read consecutive LDS words (the [jm][r] rows of the global layout are 8R bytes apart,
-  // which would put every lane of a 16-lane group on the same banks)
+  // inner-pass tables, transposed so that the lanes of a wave (consecutive jm) read
+  // consecutive LDS words (the [jm][r] rows of the global layout are 8R bytes apart, which
+  // would put every lane of a 16-lane group on the same banks): [r][jm] for a split pass,
+  // else [r / 2][jm] pairs (entries r and r + 1 side by side, one 16-byte read per pair)
   float2* small = lds + C::LDS;
   sfor<1, C::NP - 1>([&](auto pv) {
     constexpr int P = decltype(pv)::value;
@@ -623,7 +650,8 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
     constexpr int OFF = small_tw_offset<C>(P);
     for (int i = t; i < NS * RP; i += C::T) {
       const int jm = i / RP, r = i % RP;
-      small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
+      if constexpr (is_split_pass<C>(P)) small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
+      else small[OFF + 2 * ((r / 2) * NS + jm) + (r & 1)] = tw[tw_offset<C, false>(P) + i];
     }
   });
   __syncthreads();
@@ -643,20 +671,21 @@ __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) 
   constexpr int NB = C::N / R;
   constexpr int NS = ns_fwd<C>(P);
   float2 a[R];
-  const float2* rb = lds + pad(t);
-  sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+  const float2* rb = lds + pad<C>(t);
+  sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
   __syncthreads();
   const int jm = t % NS;
-  const float2* tb = lds + C::LDS + small_tw_offset<C>(P) + jm;  // table [r][jm]
-  dft_pow2_tw<R, INV>(a, [&](auto rv) { return tb[decltype(rv)::value * NS]; });
+  static_assert(R % 2 == 0 && small_tw_offset<C>(P) % 2 == 0 && C::LDS % 2 == 0, "16-byte twiddle pairs");
+  const float4* tb = reinterpret_cast<const float4*>(lds + C::LDS + small_tw_offset<C>(P)) + jm;  // [r / 2][jm]
+  dft_pow2_tw<R, INV>(a, [&](auto rv) {
+    constexpr int r = decltype(rv)::value;
+    const float4 q = tb[(r / 2) * NS];
+    return (r & 1) ? make_float2(q.z, q.w) : make_float2(q.x, q.y);
+  });
   const int idx0 = (t / NS) * NS * R + jm;
-  float2* wb = lds + pad(idx0);
-  static_assert(NS % 16 == 0 || (NS * R) % 16 == 0, "inner pass stride");
-  if constexpr (NS % 16 == 0) {
-    sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NS)] = a[decltype(qv)::value]; });
-  } else {
-    sfor<0, R>([&](auto qv) { lds[pad(idx0 + decltype(qv)::value * NS)] = a[decltype(qv)::value]; });
-  }
+  float2* wb = lds + pad<C>(idx0);
+  static_assert(pad_offsets_ok<C>(NS, R), "inner pass stride");
+  sfor<0, R>([&](auto qv) { wb[pad<C>(decltype(qv)::value * NS)] = a[decltype(qv)::value]; });
   __syncthreads();
 }
 
@@ -712,11 +741,11 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
   constexpr int QP = SS::QP;
   constexpr int H = SS::H;
   constexpr int NS = ns_fwd<C>(P);
-  static_assert(NB % 64 == 0 && NS % 16 == 0, "split pass strides");
+  static_assert(NB % 64 == 0 && NS % C::PG == 0, "split pass strides");
   const int s = __builtin_amdgcn_readfirstlane(t / NB);  // uniform across a wave
   const int j = t - s * NB;
   const float* __restrict__ cf = split_coef<R, S>.v + s * (H * QP * 2);
-  const float2* rb = lds + pad(j);
+  const float2* rb = lds + pad<C>(j);
   const float2 x0 = rb[0];
   float2 re[QP], im[QP];
   sfor<0, QP>([&](auto iv) {
@@ -726,7 +755,7 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
   float2 sum = x0;
   sfor<1, H + 1>([&](auto rv) {
     constexpr int r = decltype(rv)::value;
-    const float2 p = rb[r * pad(NB)], m = rb[(R - r) * pad(NB)];
+    const float2 p = rb[r * pad<C>(NB)], m = rb[(R - r) * pad<C>(NB)];
     const float2 sp = cadd(p, m), dm = csub(p, m);
     sum = cadd(sum, sp);
     const float* cr = cf + (r - 1) * QP * 2;
@@ -743,14 +772,14 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
   __syncthreads();
   // forward: A_q = re - i im, A_{R-q} = re + i im; the inverse swaps them
   const int q0 = s * QP + 1;
-  float2* wb = lds + pad((j / NS) * NS * R + (j % NS));
+  float2* wb = lds + pad<C>((j / NS) * NS * R + (j % NS));
   sfor<0, QP>([&](auto iv) {
     constexpr int i = decltype(iv)::value;
     const float2 minus = make_float2(re[i].x + im[i].y, re[i].y - im[i].x);
     const float2 plus = make_float2(re[i].x - im[i].y, re[i].y + im[i].x);
     if (H % QP == 0 || q0 + i <= H) {
-      wb[(q0 + i) * pad(NS)] = INV ? plus : minus;
-      wb[(R - q0 - i) * pad(NS)] = INV ? minus : plus;
+      wb[(q0 + i) * pad<C>(NS)] = INV ? plus : minus;
+      wb[(R - q0 - i) * pad<C>(NS)] = INV ? minus : plus;
     }
   });
   if (s == 0) wb[0] = sum;
@@ -774,7 +803,8 @@ __device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
 template <class C, bool INV>
 __device__ __forceinline__ void res_first_pass(float2 (&a)[C::R0], float2* lds, int t) {
   constexpr int R = C::R0;
-  float2* wb = lds + pad(t * R);
+  static_assert(C::PG % R == 0, "first pass: element q of butterfly t at slot pad(t R) + q");
+  float2* wb = lds + pad<C>(t * R);
   if constexpr (has_split_pass<C>()) {
     constexpr int NB1 = C::N / C::rad[1];
     static_assert(NB1 % R == 0 && ns_fwd<C>(1) == R, "split pass after the first pass");
@@ -786,6 +816,15 @@ __device__ __forceinline__ void res_first_pass(float2 (&a)[C::R0], float2* lds, 
       const float4 q = tb[h];
       if constexpr (h > 0) wb[2 * h] = twmul<INV>(a[2 * h], make_float2(q.x, q.y));
       wb[2 * h + 1] = twmul<INV>(a[2 * h + 1], make_float2(q.z, q.w));
+    });
+  } else if constexpr (lane_perm<C>()) {
+    static_assert(C::PW % 2 == 0 && (C::PG / R) % 2 == 0, "16-byte aligned output pairs");
+    float2 o[R];
+    dft<R, INV>(a, [&](int q, float2 v) { o[q] = v; });
+    float4* w4 = reinterpret_cast<float4*>(wb);
+    sfor<0, R / 2>([&](auto hv) {
+      constexpr int h = decltype(hv)::value;
+      w4[h] = make_float4(o[2 * h].x, o[2 * h].y, o[2 * h + 1].x, o[2 * h + 1].y);
     });
   } else {
     dft<R, INV>(a, [&](int q, float2 v) { wb[q] = v; });
@@ -799,7 +838,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   constexpr int N = C::N;
   constexpr int R = C::R0;
   constexpr int NB = N / R;
-  const int t = opaque(static_cast<int>(threadIdx.x));
+  const int t = opaque(bfly<C>(threadIdx.x));
   const bool act = (C::T == NB) || t < NB;
   // forward pass 0 (stride 1): registers -> LDS
   if (act) {
@@ -811,27 +850,27 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   res_inner_passes<C, 1, false>(lds, t);
   // forward last pass (stride N/R), fused with the eps step and the inverse first pass
   float2 y[R];
-  const float2* rb = lds + pad(t);
+  const float2* rb = lds + pad<C>(t);
   // the last pass reads and writes the same elements t + q N/R, which no other thread touches:
   // no barrier between its read and its write
-  if (act) sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+  if (act) sfor<0, R>([&](auto rv) { y[decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
   launder_powers<C>(rr);
   if (act) {
     dft_pow2_tw<R, false>(y, [&](auto rv) { return last_tw<C, decltype(rv)::value>(rr); });  // y[q] = Y_{t + q NB}
-    float2* wb = lds + pad(t);
-    sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad(NB)] = y[decltype(qv)::value]; });
+    float2* wb = lds + pad<C>(t);
+    sfor<0, R>([&](auto qv) { wb[decltype(qv)::value * pad<C>(NB)] = y[decltype(qv)::value]; });
   }
   __syncthreads();
   if (act) {
-    // partner values Y_{N - t - q NB} (slot pad(N - t) - q pad(NB); for t = 0, q = 0 the
+    // partner values Y_{N - t - q NB} (slot pad<C>(N - t) - q pad<C>(NB); for t = 0, q = 0 the
     // slot just past the buffer is read but never used: k = 0 pairs with itself)
     const float2(&f)[R] = rr.f;
-    const float2* pb = lds + pad(N - t);
+    const float2* pb = lds + pad<C>(N - t);
     sfor<0, R>([&](auto qv) {
       constexpr int q = decltype(qv)::value;
       const float2 fq = f[q];
       const float2 own = y[q];
-      const float2 oth = pb[-q * pad(NB)];
+      const float2 oth = pb[-q * pad<C>(NB)];
       const float2 v = (fq.y != 0.f) ? oth : own;
       y[q] = make_float2(fq.x * v.x - fq.y * v.y, fq.x * v.y + fq.y * v.x);
       if constexpr (q % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
@@ -845,7 +884,7 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   // inverse last pass (stride N/R): LDS -> registers
   launder_powers<C>(rr);
   if (act) {
-    sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad(NB)]; });
+    sfor<0, R>([&](auto rv) { z[decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
     dft_pow2_tw<R, true>(z, [&](auto rv) { return last_tw<C, decltype(rv)::value>(rr); });
   }
 }
@@ -877,7 +916,7 @@ __device__ __forceinline__ float2 greedy_step(float2 (&z)[C::E], float2 (&acc)[C
   const float ca = div_n<C::N>(s[0]);
   const float cb = div_n<C::N>(s[1]);
   if (trace != nullptr) {
-    const int tid = opaque(static_cast<int>(threadIdx.x));
+    const int tid = opaque(bfly<C>(threadIdx.x));
 #pragma unroll
     for (int i = 0; i < C::B0; ++i) {
       const int j = tid + C::T * i;
@@ -913,7 +952,7 @@ __device__ __forceinline__ float to_f32(__half v) { return __half2float(v); }
 // that the element offsets are recomputed rather than kept live across the loop).
 template <class C, class IT>
 __device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restrict__ w, int64_t ldw, int64_t ra,
-                                            int64_t rb, int tid = static_cast<int>(threadIdx.x)) {
+                                            int64_t rb, int tid = bfly<C>(threadIdx.x)) {
   const IT* __restrict__ pa = w + ra * ldw;
   const IT* __restrict__ pb = w + (rb >= 0 ? rb : ra) * ldw;
 #pragma unroll
@@ -936,42 +975,77 @@ __device__ __forceinline__ void load_pair_t(float2 (&z)[C::E], const IT* __restr
   }
 }
 
-// R w for both rows of the pair (the rotation fused into the load): the rows are staged in the
-// LDS buffer in row order as float2 (row a in .x, row b in .y), signed, mixed by C_b and the
-// Hadamard factor, and read back in the register layout times 1 / sqrt(2^a) -- the same
-// operations in the same order as the standalone rotation kernel.  Uses the whole buffer.
-template <class C, class IT>
-__device__ __forceinline__ void load_pair_rot_t(float2 (&z)[C::E], const IT* __restrict__ w, int64_t ldw, int64_t ra,
-                                                int64_t rb, uint64_t seed, float scale, float2* lds) {
-  constexpr int N = C::N;
-  constexpr int B = rot_odd_part(N);
-  const int tid = threadIdx.x;
-  const IT* pa = w + ra * ldw;
-  const IT* pb = w + (rb >= 0 ? rb : ra) * ldw;
-  __syncthreads();  // the buffer may still be read by the last pass of a transform
-  for (int i = tid; i < N; i += C::T) {
-    const float s = rot_sign(seed, i);
-    lds[i] = make_float2(to_f32(pa[i]) * s, rb >= 0 ? to_f32(pb[i]) * s : 0.f);
-  }
-  __syncthreads();
-  rot_odd_factor<B, false, C::T>(lds, N, tid);
-  rot_hadamard<B, C::T>(lds, N, tid);
+template <class C, class F>
+__device__ __forceinline__ void for_each_elem(F&& f, int tid = bfly<C>(threadIdx.x)) {
 #pragma unroll
-  for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
-  for_each_elem<C>([&](int e, int i) { z[e] = rv_scale(lds[i], scale); });
-  __syncthreads();  // read before the first pass overwrites the buffer
+  for (int i = 0; i < C::B0; ++i) {
+    const int j = tid + C::T * i;
+    if (j < C::NB0) {
+#pragma unroll
+      for (int r = 0; r < C::R0; ++r) f(i * C::R0 + r, orig_index<C::N>(j + r * C::NB0));
+    }
+  }
 }
 
-template <class C>
-__device__ __forceinline__ void load_pair_rot(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
-                                              int64_t rb, uint64_t seed, float scale, float2* lds) {
-  if (dtype == 1) load_pair_rot_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, seed, scale, lds);
-  else load_pair_rot_t<C>(z, static_cast<const float*>(w), ldw, ra, rb, seed, scale, lds);
+// Rows a and b of w (b if >= 0, else zeros) into the LDS buffer in row order as float2 (row a
+// in .x, row b in .y), times the rotation's sign s_i when ROT.  Each thread issues its loads in
+// batches of eight per row before the first store, so that several are in flight at once.
+template <class C, bool ROT, class IT>
+__device__ __forceinline__ void stage_pair_t(float2* lds, const IT* __restrict__ w, int64_t ldw, int64_t ra,
+                                             int64_t rb, uint64_t seed, int tid) {
+  constexpr int K = (C::N + C::T - 1) / C::T;  // entries per thread and row
+  constexpr int BATCH = 8;
+  const IT* __restrict__ pa = w + ra * ldw;
+  const IT* __restrict__ pb = w + (rb >= 0 ? rb : ra) * ldw;
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += BATCH) {
+    IT va[BATCH], vb[BATCH];
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) {
+      const int i = tid + (k0 + k) * C::T;
+      if (k0 + k < K && (C::N % C::T == 0 || i < C::N)) {
+        va[k] = pa[i];
+        vb[k] = pb[i];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) {
+      const int i = tid + (k0 + k) * C::T;
+      if (k0 + k < K && (C::N % C::T == 0 || i < C::N)) {
+        float2 v = make_float2(to_f32(va[k]), rb >= 0 ? to_f32(vb[k]) : 0.f);
+        if constexpr (ROT) v = rv_scale(v, rot_sign(seed, i));
+        lds[i] = v;
+      }
+    }
+  }
+}
+
+// w (or R w when ROT: the rotation fused into the load) for both rows of the pair, handed to
+// f(e, t) entry by entry in the greedy register layout (t = both rows' values at that entry,
+// times 1 / sqrt(2^a) when ROT).  The rows are staged in the LDS buffer in row order; for ROT
+// they are signed there and mixed by C_b and the Hadamard factor -- the operations of the
+// standalone rotation kernel in the same order.  Uses the whole buffer, with a barrier on entry
+// (a transform may still read it) and on exit (the next transform overwrites it).
+template <class C, bool ROT, class F>
+__device__ __forceinline__ void load_pair_staged(const void* w, int dtype, int64_t ldw, int64_t ra, int64_t rb,
+                                                 uint64_t seed, float scale, float2* lds, F&& f) {
+  const int tid = bfly<C>(threadIdx.x);
+  __syncthreads();
+  if (dtype == 1) stage_pair_t<C, ROT>(lds, static_cast<const __half*>(w), ldw, ra, rb, seed, tid);
+  else stage_pair_t<C, ROT>(lds, static_cast<const float*>(w), ldw, ra, rb, seed, tid);
+  __syncthreads();
+  if constexpr (ROT) {
+    constexpr int B = rot_odd_part(C::N);
+    rot_odd_factor_fixed<B, false, C::T, C::N>(lds, tid);
+    rot_hadamard<B, C::T>(lds, C::N, tid);
+  }
+  for_each_elem<C>([&](int e, int i) { f(e, ROT ? rv_scale(lds[i], scale) : lds[i]); }, tid);
+  __syncthreads();
 }
 
 template <class C>
 __device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
-                                          int64_t rb, int tid = static_cast<int>(threadIdx.x)) {
+                                          int64_t rb, int tid = bfly<C>(threadIdx.x)) {
   if (dtype == 1) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, tid);
   else load_pair_t<C>(z, static_cast<const float*>(w), ldw, ra, rb, tid);
 }
@@ -989,17 +1063,7 @@ __device__ __forceinline__ void sub_from_rows(float2 (&z)[C::E], const void* w, 
   }
 }
 
-template <class C, class F>
-__device__ __forceinline__ void for_each_elem(F&& f, int tid = static_cast<int>(threadIdx.x)) {
-#pragma unroll
-  for (int i = 0; i < C::B0; ++i) {
-    const int j = tid + C::T * i;
-    if (j < C::NB0) {
-#pragma unroll
-      for (int r = 0; r < C::R0; ++r) f(i * C::R0 + r, orig_index<C::N>(j + r * C::NB0));
-    }
-  }
-}
+
 
 // Per-row power-of-two scale s (|w| * s in [0.5, 1)) and a NaN/Inf flag, for both rows.
 // Returns the scales and zeroes a row that is not finite.
@@ -1189,8 +1253,14 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   };
 
   float2 z[C::E], vh[C::E];
-  if constexpr (ROT) load_pair_rot<C>(z, a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds);
-  else load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
+  if constexpr (ROT) {
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
+    load_pair_staged<C, true>(a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds,
+                              [&](int e, float2 t) { z[e] = t; });
+  } else {
+    load_pair<C>(z, a.w, a.dtype, a.ldw, ra, rb);
+  }
   float2 scale, unscale;
   bool bad_a, bad_b;
   normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
@@ -1272,13 +1342,10 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   for (int e = 0; e < C::E; ++e) z[e] = cadd(z[e], vh[e]);
   applyP(z);
   if constexpr (ROT) {
-    float2 t[C::E];
-    load_pair_rot<C>(t, a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds);
-#pragma unroll
-    for (int e = 0; e < C::E; ++e) {
-      z[e].x = bad_a ? 0.f : fmaf(t[e].x, scale.x, -z[e].x);
-      z[e].y = bad_b ? 0.f : fmaf(t[e].y, scale.y, -z[e].y);
-    }
+    load_pair_staged<C, true>(a.w, a.dtype, a.ldw, ra, rb, a.rot_seed, a.rot_scale, lds, [&](int e, float2 t) {
+      z[e].x = bad_a ? 0.f : fmaf(t.x, scale.x, -z[e].x);
+      z[e].y = bad_b ? 0.f : fmaf(t.y, scale.y, -z[e].y);
+    });
   } else {
     sub_from_rows<C>(z, a.w, a.dtype, a.ldw, ra, rb, scale, bad_a, bad_b);
   }
@@ -1378,7 +1445,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   for (int64_t it = blockIdx.x; it < nitems; it += gridDim.x) {
     const int64_t ra = 2 * (item0 + it);
     const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
-    const int tid = opaque(static_cast<int>(threadIdx.x));
+    const int tid = opaque(bfly<C>(threadIdx.x));
     float2 z[C::E];
 #pragma unroll
     for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
@@ -1453,7 +1520,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
       }
       __syncthreads();
       rot_hadamard<B, C::T>(lds, N, tid);
-      rot_odd_factor<B, true, C::T>(lds, N, tid);
+      rot_odd_factor_fixed<B, true, C::T, N>(lds, tid);
       float* ya = a.y + ra * a.ldy;
       float* yb = a.y + (rb >= 0 ? rb : ra) * a.ldy;
       for (int i = tid; i < N; i += C::T) {
@@ -1601,7 +1668,7 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
     cb = act_b ? cb : 0.f;
     if (tracing) {
       const bool vs = side ? vb : va;
-      const int tid = opaque(static_cast<int>(threadIdx.x));
+      const int tid = opaque(bfly<C>(threadIdx.x));
       int8_t* trs = a.tr_signs + (item * steps + st) * int64_t(C::N);
 #pragma unroll
       for (int i = 0; i < C::B0; ++i) {

@@ -58,24 +58,97 @@ __device__ __forceinline__ void rot_odd_factor(V* buf, int n, int tid) {
   }
 }
 
-// unnormalised Walsh-Hadamard transform over the 2^a segments (stride B), in place, radix-2
-// stages with a barrier after each
-template <int B, int T, class V>
-__device__ __forceinline__ void rot_hadamard(V* buf, int n, int tid) {
-  const int p2 = n / B;
-  for (int lh = 0; (1 << lh) < p2; ++lh) {
-    const int h = 1 << lh;
-    for (int t = tid; t < n / 2; t += T) {
-      const int q = t / B, j = t - q * B;  // butterfly q of the stage, column j
-      const int i0 = ((q >> lh) << (lh + 1)) | (q & (h - 1));
-      V* p0 = buf + i0 * B + j;
-      V* p1 = p0 + h * B;
-      const V a = *p0, b = *p1;
-      *p0 = rv_add(a, b);
-      *p1 = rv_sub(a, b);
+// outputs K0 .. K0 + KC - 1 (those below B) of C_B seg (or C_B^T seg), each accumulated over the
+// inputs in ascending order from zero, as rot_odd_segment does
+template <int B, bool TRANS, int K0, int KC, class V>
+__device__ __forceinline__ void rot_odd_chunk(const V* seg, V (&acc)[KC]) {
+#pragma unroll
+  for (int kk = 0; kk < KC; ++kk) acc[kk] = rv_zero(acc[0]);
+#pragma unroll
+  for (int j = 0; j < B; ++j) {
+    const V x = seg[j];
+#pragma unroll
+    for (int kk = 0; kk < KC; ++kk) {
+      if (K0 + kk < B)
+        acc[kk] = rv_fma(TRANS ? DctTab<B>::m[j * B + K0 + kk] : DctTab<B>::m[(K0 + kk) * B + j], x, acc[kk]);
+    }
+  }
+}
+
+// The odd factor for a length N known at compile time.  When the workgroup has at least twice
+// as many threads as segments and B is large, each segment's outputs are split into NC chunks
+// computed by NC threads (all inputs read before the barrier, outputs written after it), so that
+// more waves share the work and each holds fewer values; otherwise one thread per segment.
+template <int B, bool TRANS, int T, int N, class V>
+__device__ __forceinline__ void rot_odd_factor_fixed(V* buf, int tid) {
+  constexpr int NSEG = N / B;
+  constexpr int NC = (B >= 16 && T >= 2 * NSEG) ? (T / NSEG < 3 ? T / NSEG : 3) : 1;
+  if constexpr (NC == 1) {
+    rot_odd_factor<B, TRANS, T>(buf, N, tid);
+  } else {
+    constexpr int KC = (B + NC - 1) / NC;
+    V acc[KC];
+    const int c = tid / NSEG, sg = tid - c * NSEG;  // chunk and segment of this thread
+    const V* seg = buf + sg * B;
+    if (c == 0) {
+      rot_odd_chunk<B, TRANS, 0, KC>(seg, acc);
+    } else if (c == 1) {
+      rot_odd_chunk<B, TRANS, KC, KC>(seg, acc);
+    } else if (NC == 3 && c == 2) {
+      rot_odd_chunk<B, TRANS, 2 * KC, KC>(seg, acc);
+    }
+    __syncthreads();  // every input read before any output is written
+    if (c < NC) {
+      V* out = buf + sg * B + c * KC;
+#pragma unroll
+      for (int kk = 0; kk < KC; ++kk)
+        if (c * KC + kk < B) out[kk] = acc[kk];
     }
     __syncthreads();
   }
+}
+
+// One pass of the unnormalised Walsh-Hadamard transform over the segment-index bits
+// [lh, lh + log2 R): each thread takes groups of R entries at stride 2^lh B, transforms them in
+// registers with radix-2 stages in ascending bit order, and writes them back; then a barrier.
+// Consecutive threads take consecutive offsets within a stride, so each access is contiguous.
+template <int B, int R, int T, class V>
+__device__ __forceinline__ void rot_hadamard_pass(V* buf, int n, int lh, int tid) {
+  const int hb = (1 << lh) * B;
+  for (int q = tid; q < n / R; q += T) {
+    const int hi = (q >> lh) / B;  // = q / hb
+    V* p = buf + hi * (R * hb) + (q - hi * hb);
+    V x[R];
+#pragma unroll
+    for (int m = 0; m < R; ++m) x[m] = p[m * hb];
+#pragma unroll
+    for (int st = 1; st < R; st <<= 1) {
+#pragma unroll
+      for (int m = 0; m < R; ++m) {
+        if (!(m & st)) {
+          const V u = x[m], v = x[m + st];
+          x[m] = rv_add(u, v);
+          x[m + st] = rv_sub(u, v);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < R; ++m) p[m * hb] = x[m];
+  }
+  __syncthreads();
+}
+
+// unnormalised Walsh-Hadamard transform over the 2^a segments (stride B), in place: passes of
+// radix 16 (a last one of radix 2, 4 or 8), the radix-2 stages in ascending bit order overall
+template <int B, int T, class V>
+__device__ __forceinline__ void rot_hadamard(V* buf, int n, int tid) {
+  const int a = __builtin_ctz(static_cast<unsigned>(n));  // n = 2^a B, B odd
+  int lh = 0;
+  for (; lh + 4 <= a; lh += 4) rot_hadamard_pass<B, 16, T>(buf, n, lh, tid);
+  const int r = a - lh;
+  if (r == 3) rot_hadamard_pass<B, 8, T>(buf, n, lh, tid);
+  else if (r == 2) rot_hadamard_pass<B, 4, T>(buf, n, lh, tid);
+  else if (r == 1) rot_hadamard_pass<B, 2, T>(buf, n, lh, tid);
 }
 
 // b, the odd part of n = 2^a b
