@@ -74,7 +74,7 @@ void make_signs(int32_t n, uint64_t seed, int8_t* out) {
 //  mid: for the first inverse pass (radix R = last forward radix, stride 1), entry j R + r
 //       for element k = j + r n/R: Y'_k = f_k Y_s(k) with s(k) = k and f_k = eps_k / n when
 //       eps_k == eps_{n-k} (k = 0 and k = n/2 pair with themselves), else s(k) = n - k and
-//       f_k = eps_k exp(i pi k / n) / n; stored as {Re f, Im f, LDS byte address of s(k), 0}.
+//       f_k = eps_k exp(i pi k / n) / n; stored as {Re f, Im f, LDS byte address of s(k), eps_k}.
 void build_tables(int n, const int8_t* eps, std::vector<float2>* tw, std::vector<float4>* mid) {
   kashin::PlanShape sh;
   kashin::plan_shape(n, &sh);
@@ -121,7 +121,7 @@ void build_tables(int n, const int8_t* eps, std::vector<float2>* tw, std::vector
       const int addr = kashin::pad_slot(n, wide, src) * int(sizeof(float2));
       float faddr;
       std::memcpy(&faddr, &addr, sizeof(faddr));
-      (*mid)[j * R + r] = make_float4(fx, fy, faddr, 0.f);
+      (*mid)[j * R + r] = make_float4(fx, fy, faddr, float(ek));
     }
 }
 

@@ -584,10 +584,57 @@ constexpr int small_tw_total() {
   return resident_ok<C>() ? small_tw_offset<C>(C::NP - 1) : 0;
 }
 
+// eps factors f_k of the fused step for the thread's elements k = t + q N/R: kept as R complex
+// values, or -- for the split shape, whose block loop is register-bound -- as e^{i pi t/N}/N and
+// a mask (bit 2q: eps_k < 0, bit 2q + 1: eps_k != eps_{N-k}), from which f_k = eps_k / N or
+// eps_k e^{i pi k/N} / N = eps_k (e^{i pi t/N} / N) e^{i pi q/R} is rebuilt at each use.
+template <class C>
+constexpr bool compact_eps() {
+  return has_split_pass<C>();
+}
+template <class C, bool COMPACT = compact_eps<C>()>
+struct EpsRegs {
+  float2 f[C::R0];
+};
+template <class C>
+struct EpsRegs<C, true> {
+  float2 base;
+  uint32_t bits;
+};
+// e^{i pi q / 16}
+struct Half32 {
+  static constexpr double c[16] = {1.0, 0.9807852804032304, 0.9238795325112867, 0.8314696123025452,
+                                   0.7071067811865476, 0.5555702330196023, 0.38268343236508984, 0.19509032201612833,
+                                   0.0, -0.1950903220161282, -0.3826834323650897, -0.555570233019602,
+                                   -0.7071067811865475, -0.8314696123025453, -0.9238795325112867, -0.9807852804032304};
+  static constexpr double s[16] = {0.0, 0.19509032201612825, 0.3826834323650898, 0.5555702330196022,
+                                   0.7071067811865475, 0.8314696123025452, 0.9238795325112867, 0.9807852804032304,
+                                   1.0, 0.9807852804032304, 0.9238795325112867, 0.8314696123025455,
+                                   0.7071067811865476, 0.5555702330196022, 0.3826834323650899, 0.1950903220161286};
+};
+// f_k for element q, and whether it takes the partner value (eps_k != eps_{N-k})
+template <class C, int q>
+__device__ __forceinline__ float2 eps_factor(const EpsRegs<C>& e, bool& partner) {
+  if constexpr (compact_eps<C>()) {
+    static_assert(C::R0 == 16, "compact eps factors assume radix 16");
+    partner = (e.bits >> (2 * q + 1)) & 1u;
+    const bool neg = (e.bits >> (2 * q)) & 1u;
+    constexpr float cx = static_cast<float>(Half32::c[q]), cy = static_cast<float>(Half32::s[q]);
+    constexpr float inv_n = static_cast<float>(1.0 / C::N);
+    const float2 g = partner ? make_float2(e.base.x * cx - e.base.y * cy, e.base.x * cy + e.base.y * cx)
+                             : make_float2(inv_n, 0.f);
+    return neg ? make_float2(-g.x, -g.y) : g;
+  } else {
+    const float2 f = e.f[q];
+    partner = f.y != 0.f;
+    return f;
+  }
+}
+
 template <class C>
 struct ResRegs {
   float2 tw[C::R0];  // w_N^(r t) for r in {1, 2, 3, 4, 8, 12}: the rest are products of two of these
-  float2 f[C::R0];   // eps factors of the fused step for elements k = t + r N/R
+  EpsRegs<C> eps;    // eps factors of the fused step for elements k = t + r N/R
 };
 
 // twiddle r of the last pass from the stored powers (R = 16: r = 4a + b, w_r = w_4a * w_b)
@@ -614,6 +661,8 @@ __device__ __forceinline__ void launder_powers(ResRegs<C>& rr) {
                    "+v"(rr.tw[3].y), "+v"(rr.tw[4].x), "+v"(rr.tw[4].y), "+v"(rr.tw[8].x), "+v"(rr.tw[8].y),
                    "+v"(rr.tw[12].x), "+v"(rr.tw[12].y));
   }
+  // the compact eps factors are rebuilt inside the block loop, not hoisted out of it as R live values
+  if constexpr (compact_eps<C>()) asm volatile("" : "+v"(rr.eps.base.x), "+v"(rr.eps.base.y), "+v"(rr.eps.bits));
 }
 
 template <class C>
@@ -634,10 +683,24 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
       if constexpr (keep1) rr.tw[2 * h + 1] = make_float2(q.z, q.w);
     }
   });
-  sfor<0, R>([&](auto rv) {
-    const float4 m = mid[tl * R + decltype(rv)::value];
-    rr.f[decltype(rv)::value] = make_float2(m.x, m.y);
-  });
+  if constexpr (compact_eps<C>()) {
+    uint32_t bits = 0;
+    sfor<0, R>([&](auto rv) {
+      constexpr int q = decltype(rv)::value;
+      const float4 m = mid[tl * R + q];  // {Re f_k, Im f_k, -, eps_k}
+      bits |= (m.w < 0.f ? 1u : 0u) << (2 * q);
+      bits |= (m.y != 0.f ? 1u : 0u) << (2 * q + 1);
+    });
+    float sn, cs;
+    sincospif(static_cast<float>(tl) / static_cast<float>(C::N), &sn, &cs);
+    rr.eps.bits = bits;
+    rr.eps.base = make_float2(cs * static_cast<float>(1.0 / C::N), sn * static_cast<float>(1.0 / C::N));
+  } else {
+    sfor<0, R>([&](auto rv) {
+      const float4 m = mid[tl * R + decltype(rv)::value];
+      rr.eps.f[decltype(rv)::value] = make_float2(m.x, m.y);
+    });
+  }
   // inner-pass tables, transposed so that the lanes of a wave (consecutive jm) read
   // consecutive LDS words (the [jm][r] rows of the global layout are 8R bytes apart, which
   // would put every lane of a 16-lane group on the same banks): [r][jm] for a split pass,
@@ -864,14 +927,14 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResR
   if (act) {
     // partner values Y_{N - t - q NB} (slot pad<C>(N - t) - q pad<C>(NB); for t = 0, q = 0 the
     // slot just past the buffer is read but never used: k = 0 pairs with itself)
-    const float2(&f)[R] = rr.f;
     const float2* pb = lds + pad<C>(N - t);
     sfor<0, R>([&](auto qv) {
       constexpr int q = decltype(qv)::value;
-      const float2 fq = f[q];
+      bool partner;
+      const float2 fq = eps_factor<C, q>(rr.eps, partner);
       const float2 own = y[q];
       const float2 oth = pb[-q * pad<C>(NB)];
-      const float2 v = (fq.y != 0.f) ? oth : own;
+      const float2 v = partner ? oth : own;
       y[q] = make_float2(fq.x * v.x - fq.y * v.y, fq.x * v.y + fq.y * v.x);
       if constexpr (q % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound partner values in flight
     });
