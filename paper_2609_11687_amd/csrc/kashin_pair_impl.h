@@ -585,14 +585,15 @@ constexpr int small_tw_total() {
 }
 
 // eps factors f_k of the fused step for the thread's elements k = t + q N/R: kept as R complex
-// values, or -- for the split shape, whose block loop is register-bound -- as e^{i pi t/N}/N and
-// a mask (bit 2q: eps_k < 0, bit 2q + 1: eps_k != eps_{N-k}), from which f_k = eps_k / N or
-// eps_k e^{i pi k/N} / N = eps_k (e^{i pi t/N} / N) e^{i pi q/R} is rebuilt at each use.
+// values, or -- COMPACT, for kernels whose block loop is register-bound on the split shape -- as
+// e^{i pi t/N}/N and a mask (bit 2q: eps_k < 0, bit 2q + 1: eps_k != eps_{N-k}), from which
+// f_k = eps_k / N or eps_k e^{i pi k/N} / N = eps_k (e^{i pi t/N} / N) e^{i pi q/R} is rebuilt at
+// each use.
 template <class C>
 constexpr bool compact_eps() {
   return has_split_pass<C>();
 }
-template <class C, bool COMPACT = compact_eps<C>()>
+template <class C, bool COMPACT>
 struct EpsRegs {
   float2 f[C::R0];
 };
@@ -613,9 +614,9 @@ struct Half32 {
                                    0.7071067811865476, 0.5555702330196022, 0.3826834323650899, 0.1950903220161286};
 };
 // f_k for element q, and whether it takes the partner value (eps_k != eps_{N-k})
-template <class C, int q>
-__device__ __forceinline__ float2 eps_factor(const EpsRegs<C>& e, bool& partner) {
-  if constexpr (compact_eps<C>()) {
+template <class C, int q, bool COMPACT>
+__device__ __forceinline__ float2 eps_factor(const EpsRegs<C, COMPACT>& e, bool& partner) {
+  if constexpr (COMPACT) {
     static_assert(C::R0 == 16, "compact eps factors assume radix 16");
     partner = (e.bits >> (2 * q + 1)) & 1u;
     const bool neg = (e.bits >> (2 * q)) & 1u;
@@ -631,15 +632,16 @@ __device__ __forceinline__ float2 eps_factor(const EpsRegs<C>& e, bool& partner)
   }
 }
 
-template <class C>
+template <class C, bool COMPACT = false>
 struct ResRegs {
-  float2 tw[C::R0];  // w_N^(r t) for r in {1, 2, 3, 4, 8, 12}: the rest are products of two of these
-  EpsRegs<C> eps;    // eps factors of the fused step for elements k = t + r N/R
+  static constexpr bool compact = COMPACT;
+  float2 tw[C::R0];         // w_N^(r t) for r in {1, 2, 3, 4, 8, 12}: the rest are products of two of these
+  EpsRegs<C, COMPACT> eps;  // eps factors of the fused step for elements k = t + r N/R
 };
 
 // twiddle r of the last pass from the stored powers (R = 16: r = 4a + b, w_r = w_4a * w_b)
-template <class C, int r>
-__device__ __forceinline__ float2 last_tw(const ResRegs<C>& rr) {
+template <class C, int r, class RR>
+__device__ __forceinline__ float2 last_tw(const RR& rr) {
   if constexpr (C::R0 < 16 || r <= 4 || r == 8 || r == 12) {
     return rr.tw[r];
   } else {
@@ -653,8 +655,8 @@ __device__ __forceinline__ float2 last_tw(const ResRegs<C>& rr) {
 // the products formed from them are neither hoisted out of the block loop nor shared between
 // the two last passes of one application of P, either of which would keep nine more complex
 // values live.
-template <class C>
-__device__ __forceinline__ void launder_powers(ResRegs<C>& rr) {
+template <class C, class RR>
+__device__ __forceinline__ void launder_powers(RR& rr) {
   if constexpr (C::R0 == 16) {
     asm volatile(""
                  : "+v"(rr.tw[1].x), "+v"(rr.tw[1].y), "+v"(rr.tw[2].x), "+v"(rr.tw[2].y), "+v"(rr.tw[3].x),
@@ -662,11 +664,11 @@ __device__ __forceinline__ void launder_powers(ResRegs<C>& rr) {
                    "+v"(rr.tw[12].x), "+v"(rr.tw[12].y));
   }
   // the compact eps factors are rebuilt inside the block loop, not hoisted out of it as R live values
-  if constexpr (compact_eps<C>()) asm volatile("" : "+v"(rr.eps.base.x), "+v"(rr.eps.base.y), "+v"(rr.eps.bits));
+  if constexpr (RR::compact) asm volatile("" : "+v"(rr.eps.base.x), "+v"(rr.eps.base.y), "+v"(rr.eps.bits));
 }
 
-template <class C>
-__device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const float2* __restrict__ tw,
+template <class C, class RR>
+__device__ __forceinline__ void resident_load(RR& rr, float2* lds, const float2* __restrict__ tw,
                                               const float4* __restrict__ mid) {
   constexpr int R = C::R0;
   constexpr int NB = C::N / R;
@@ -683,7 +685,7 @@ __device__ __forceinline__ void resident_load(ResRegs<C>& rr, float2* lds, const
       if constexpr (keep1) rr.tw[2 * h + 1] = make_float2(q.z, q.w);
     }
   });
-  if constexpr (compact_eps<C>()) {
+  if constexpr (RR::compact) {
     uint32_t bits = 0;
     sfor<0, R>([&](auto rv) {
       constexpr int q = decltype(rv)::value;
@@ -896,8 +898,8 @@ __device__ __forceinline__ void res_first_pass(float2 (&a)[C::R0], float2* lds, 
 
 // z <- P z on the resident path.  Threads past the last radix-R0 butterfly (T > N/R0, only
 // with a split pass) take part in the split pass and the barriers only.
-template <class C>
-__device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, ResRegs<C>& rr) {
+template <class C, class RR>
+__device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, RR& rr) {
   constexpr int N = C::N;
   constexpr int R = C::R0;
   constexpr int NB = N / R;
@@ -1308,7 +1310,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   int slot = 0;
 
   constexpr bool RES = resident_ok<C>();
-  ResRegs<C> rr;
+  ResRegs<C, compact_eps<C>()> rr;
   if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
   auto applyP = [&](float2(&v)[C::E]) {
     if constexpr (RES) apply_P_res<C>(v, lds, rr);
@@ -1670,7 +1672,7 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
   const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
   int slot = 0;
   constexpr bool RES = resident_ok<C>();
-  ResRegs<C> rr;
+  ResRegs<C, compact_eps<C>()> rr;
   if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
   auto applyP = [&](float2(&v)[C::E]) {
     if constexpr (RES) apply_P_res<C>(v, lds, rr);
