@@ -276,6 +276,14 @@ constexpr bool pad_offsets_ok(int S, int R) {
   return S % C::PG == 0 || (C::PG % S == 0 && ((S * R) % C::PG == 0 || C::PG % (S * R) == 0));
 }
 
+// Opaque copy of the thread index: without it every twiddle load and LDS address of every
+// pass is proven invariant across the block loop, hoisted out of it, and kept live in
+// registers at once.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 // Butterfly index of thread l.  With two spare slots per 32 elements the resident transform
 // gives the butterflies of each 16-lane group to its lanes in the order 0, 2, .., 14, 1, 3, ..,
 // 15: the first pass then writes its outputs 16t + q, q < 16, as 16-byte pairs, and the eight
@@ -287,17 +295,14 @@ constexpr bool lane_perm() {
 }
 template <class C>
 __device__ __forceinline__ int bfly(int l) {
-  if constexpr (lane_perm<C>()) return (l & ~15) | (2 * (l & 7)) | ((l >> 3) & 1);
-  else return l;
+  if constexpr (lane_perm<C>()) {
+    const int m = opaque(l);  // recomputed at each use rather than kept live (or spilled) across the kernel
+    return (m & ~15) | (2 * (m & 7)) | ((m >> 3) & 1);
+  } else {
+    return l;
+  }
 }
 
-// Opaque copy of the thread index: without it every twiddle load and LDS address of every
-// pass is proven invariant across the block loop, hoisted out of it, and kept live in
-// registers at once.
-__device__ __forceinline__ int opaque(int v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
 
 // Position m of the even/odd order -> index in the row.
 template <int N>
