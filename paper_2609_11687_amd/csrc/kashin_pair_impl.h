@@ -590,7 +590,8 @@ constexpr int small_tw_total() {
 }
 
 // eps factors f_k of the fused step for the thread's elements k = t + q N/R: kept as R complex
-// values, or -- COMPACT, for kernels whose block loop is register-bound on the split shape -- as
+// values, or -- COMPACT, for kernels whose block loop is register-bound on the split shape (which
+// also keep only powers 1 and 4 of the last-pass twiddle, see stored_tw) -- as
 // e^{i pi t/N}/N and a mask (bit 2q: eps_k < 0, bit 2q + 1: eps_k != eps_{N-k}), from which
 // f_k = eps_k / N or eps_k e^{i pi k/N} / N = eps_k (e^{i pi t/N} / N) e^{i pi q/R} is rebuilt at
 // each use.
@@ -645,14 +646,25 @@ struct ResRegs {
 };
 
 // twiddle r of the last pass from the stored powers (R = 16: r = 4a + b, w_r = w_4a * w_b)
+__device__ __forceinline__ float2 cmulf(float2 x, float2 y) {
+  return make_float2(x.x * y.x - x.y * y.y, x.x * y.y + x.y * y.x);
+}
+// stored power r of w_N^t: all six kept, or (compact) only r = 1 and 4 with 2, 3, 8, 12 derived
+template <class C, int r, class RR>
+__device__ __forceinline__ float2 stored_tw(const RR& rr) {
+  if constexpr (!RR::compact || r == 1 || r == 4) return rr.tw[r];
+  else if constexpr (r == 2) return cmulf(rr.tw[1], rr.tw[1]);
+  else if constexpr (r == 3) return cmulf(stored_tw<C, 2>(rr), rr.tw[1]);
+  else if constexpr (r == 8) return cmulf(rr.tw[4], rr.tw[4]);
+  else return cmulf(stored_tw<C, 8>(rr), rr.tw[4]);  // r == 12
+}
 template <class C, int r, class RR>
 __device__ __forceinline__ float2 last_tw(const RR& rr) {
   if constexpr (C::R0 < 16 || r <= 4 || r == 8 || r == 12) {
-    return rr.tw[r];
+    return stored_tw<C, r>(rr);
   } else {
     constexpr int hi = r & ~3, lo = r & 3;
-    const float2 x = rr.tw[hi], y = rr.tw[lo];
-    return make_float2(x.x * y.x - x.y * y.y, x.x * y.y + x.y * y.x);
+    return cmulf(stored_tw<C, hi>(rr), stored_tw<C, lo>(rr));
   }
 }
 
@@ -663,10 +675,13 @@ __device__ __forceinline__ float2 last_tw(const RR& rr) {
 template <class C, class RR>
 __device__ __forceinline__ void launder_powers(RR& rr) {
   if constexpr (C::R0 == 16) {
-    asm volatile(""
-                 : "+v"(rr.tw[1].x), "+v"(rr.tw[1].y), "+v"(rr.tw[2].x), "+v"(rr.tw[2].y), "+v"(rr.tw[3].x),
-                   "+v"(rr.tw[3].y), "+v"(rr.tw[4].x), "+v"(rr.tw[4].y), "+v"(rr.tw[8].x), "+v"(rr.tw[8].y),
-                   "+v"(rr.tw[12].x), "+v"(rr.tw[12].y));
+    if constexpr (RR::compact)
+      asm volatile("" : "+v"(rr.tw[1].x), "+v"(rr.tw[1].y), "+v"(rr.tw[4].x), "+v"(rr.tw[4].y));
+    else
+      asm volatile(""
+                   : "+v"(rr.tw[1].x), "+v"(rr.tw[1].y), "+v"(rr.tw[2].x), "+v"(rr.tw[2].y), "+v"(rr.tw[3].x),
+                     "+v"(rr.tw[3].y), "+v"(rr.tw[4].x), "+v"(rr.tw[4].y), "+v"(rr.tw[8].x), "+v"(rr.tw[8].y),
+                     "+v"(rr.tw[12].x), "+v"(rr.tw[12].y));
   }
   // the compact eps factors are rebuilt inside the block loop, not hoisted out of it as R live values
   if constexpr (RR::compact) asm volatile("" : "+v"(rr.eps.base.x), "+v"(rr.eps.base.y), "+v"(rr.eps.bits));
