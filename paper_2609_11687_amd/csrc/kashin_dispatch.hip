@@ -12,13 +12,13 @@ namespace kashin {
   X(256, 64, 2, 16, 16)             \
   X(512, 64, 4, 8, 8, 8)            \
   X(768, 64, 3, 16, 16, 3)          \
-  X(1024, 64, 2, 16, 16, 4)         \
-  X(2048, 128, 2, 16, 16, 8)        \
+  X(1024, 64, 2, 16, 4, 16)         \
+  X(2048, 128, 2, 16, 8, 16)        \
   X(3072, 192, 3, 16, 16, 4, 3)     \
   X(4096, 256, 3, 16, 16, 16)       \
   X(8192, 512, 2, 16, 16, 16, 2)    \
   X(11008, 768, 3, 16, 43, 16)      \
-  X(16384, 1024, 4, 16, 16, 16, 4)
+  X(16384, 1024, 4, 16, 8, 8, 16)
 
 #define X(N, ...) hipError_t launch_n##N(const KArgs& a, int64_t grid, hipStream_t stream);
 KASHIN_SIZES(X)

@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(1024, 64, 2, 16, 16, 4)
+KASHIN_DEFINE_SIZE(1024, 64, 2, 16, 4, 16)
 }  // namespace kashin

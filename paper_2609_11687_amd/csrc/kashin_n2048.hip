@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(2048, 128, 2, 16, 16, 8)
+KASHIN_DEFINE_SIZE(2048, 128, 2, 16, 8, 16)
 }  // namespace kashin

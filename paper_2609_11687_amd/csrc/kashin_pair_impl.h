@@ -567,14 +567,22 @@ template <class C>
 constexpr bool has_split_pass() {
   return C::NP == 3 && is_split_pass<C>(1);
 }
+// Resident shapes: first and last radix R0 (a power of two <= 16), one butterfly of those passes
+// per thread, and either a split inner pass or inner radices that are powers of two dividing R0
+// in a palindromic sequence (so that the inverse transform meets the same radices and strides,
+// and reuses the forward twiddle tables conjugated); an inner pass of radix R gives each thread
+// R0 / R butterflies.
 template <class C>
 constexpr bool resident_ok() {
   constexpr int R0 = C::R0;
   if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % C::PG == 0))
     return false;
   if (has_split_pass<C>()) return C::T >= C::N / R0;
-  for (int p = 0; p < C::NP; ++p)
-    if (C::rad[p] != R0) return false;
+  for (int p = 0; p < C::NP; ++p) {
+    const int r = C::rad[p];
+    if (r < 2 || (r & (r - 1)) != 0 || R0 % r != 0 || r != C::rad[C::NP - 1 - p]) return false;
+    if ((C::N / r) % C::PG != 0) return false;
+  }
   return C::T == C::N / R0;
 }
 // LDS slots (float2) of the inner-pass twiddle tables (passes 1 .. NP-2), after the FFT buffer
@@ -597,7 +605,7 @@ constexpr int small_tw_total() {
 // each use.
 template <class C>
 constexpr bool compact_eps() {
-  return has_split_pass<C>();
+  return has_split_pass<C>() || (C::W >= 4 && C::R0 == 16);  // split shape, or a 128-register budget
 }
 template <class C, bool COMPACT>
 struct EpsRegs {
@@ -748,29 +756,38 @@ __device__ __forceinline__ float2 twmul(float2 v, float2 t) {
   else return make_float2(v.x * t.x + v.y * t.y, v.y * t.x - v.x * t.y);
 }
 
-// Inner pass p (1 <= p <= NP-2) of the resident path: stride NS = R^p, LDS -> LDS,
-// twiddles from the LDS copy of the pass-p table.
+// Inner pass p (1 <= p <= NP-2) of the resident path: radix R = rad[p], stride NS = the
+// product of the radices before it, LDS -> LDS, twiddles from the LDS copy of the pass-p table;
+// thread t takes butterflies t + T i, i < R0 / R.
 template <class C, int P, bool INV>
 __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) {
-  constexpr int R = C::R0;
+  constexpr int R = C::rad[P];
   constexpr int NB = C::N / R;
   constexpr int NS = ns_fwd<C>(P);
-  float2 a[R];
-  const float2* rb = lds + pad<C>(t);
-  sfor<0, R>([&](auto rv) { a[decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
-  __syncthreads();
-  const int jm = t % NS;
-  static_assert(R % 2 == 0 && small_tw_offset<C>(P) % 2 == 0 && C::LDS % 2 == 0, "16-byte twiddle pairs");
-  const float4* tb = reinterpret_cast<const float4*>(lds + C::LDS + small_tw_offset<C>(P)) + jm;  // [r / 2][jm]
-  dft_pow2_tw<R, INV>(a, [&](auto rv) {
-    constexpr int r = decltype(rv)::value;
-    const float4 q = tb[(r / 2) * NS];
-    return (r & 1) ? make_float2(q.z, q.w) : make_float2(q.x, q.y);
+  constexpr int BPT = NB / C::T;
+  static_assert(BPT * C::T == NB && BPT * R == C::R0, "inner pass butterflies per thread");
+  float2 a[BPT][R];
+  sfor<0, BPT>([&](auto iv) {
+    constexpr int i = decltype(iv)::value;
+    const float2* rb = lds + pad<C>(t + C::T * i);
+    sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
   });
-  const int idx0 = (t / NS) * NS * R + jm;
-  float2* wb = lds + pad<C>(idx0);
+  __syncthreads();
+  static_assert(R % 2 == 0 && small_tw_offset<C>(P) % 2 == 0 && C::LDS % 2 == 0, "16-byte twiddle pairs");
   static_assert(pad_offsets_ok<C>(NS, R), "inner pass stride");
-  sfor<0, R>([&](auto qv) { wb[pad<C>(decltype(qv)::value * NS)] = a[decltype(qv)::value]; });
+  sfor<0, BPT>([&](auto iv) {
+    constexpr int i = decltype(iv)::value;
+    const int j = t + C::T * i;
+    const int jm = j % NS;
+    const float4* tb = reinterpret_cast<const float4*>(lds + C::LDS + small_tw_offset<C>(P)) + jm;  // [r / 2][jm]
+    dft_pow2_tw<R, INV>(a[i], [&](auto rv) {
+      constexpr int r = decltype(rv)::value;
+      const float4 q = tb[(r / 2) * NS];
+      return (r & 1) ? make_float2(q.z, q.w) : make_float2(q.x, q.y);
+    });
+    float2* wb = lds + pad<C>((j / NS) * NS * R + jm);
+    sfor<0, R>([&](auto qv) { wb[pad<C>(decltype(qv)::value * NS)] = a[i][decltype(qv)::value]; });
+  });
   __syncthreads();
 }
 
@@ -874,7 +891,7 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
 template <class C, int P, bool INV>
 __device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
   if constexpr (P >= 1 && P <= C::NP - 2) {
-    // the inverse FFT meets the strides in the same order (R, R^2, ...) as the forward one
+    // the radices are palindromic: the inverse FFT meets the same radices and strides as the forward one
     if constexpr (is_split_pass<C>(P)) split_pass<C, P, INV>(lds, t);
     else res_inner_pass<C, P, INV>(lds, t);
     res_inner_passes<C, P + 1, INV>(lds, t);
