@@ -11,7 +11,7 @@ namespace kashin {
   X(172, 64, 2, 4, 43)              \
   X(256, 64, 2, 16, 16)             \
   X(512, 64, 4, 8, 8, 8)            \
-  X(768, 64, 3, 16, 16, 3)          \
+  X(768, 64, 3, 16, 3, 16)          \
   X(1024, 64, 2, 16, 4, 16)         \
   X(2048, 128, 2, 16, 8, 16)        \
   X(3072, 192, 3, 16, 16, 4, 3)     \

@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(768, 64, 3, 16, 16, 3)
+KASHIN_DEFINE_SIZE(768, 64, 3, 16, 3, 16)
 }  // namespace kashin

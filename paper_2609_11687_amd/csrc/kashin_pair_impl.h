@@ -567,6 +567,14 @@ template <class C>
 constexpr bool has_split_pass() {
   return C::NP == 3 && is_split_pass<C>(1);
 }
+// An inner pass of odd radix R < R0 between two radix-R0 passes (N = R0 R R0): its N/R
+// butterflies spread evenly over the T >= N/R0 threads, each read once and transformed by one
+// thread with its twiddles applied to the inputs.
+template <class C>
+constexpr bool is_odd_inner_pass(int p) {
+  const int R = C::rad[p];
+  return C::NP == 3 && p == 1 && R % 2 == 1 && R < C::R0 && C::T % 64 == 0 && (C::N / R) % C::T == 0;
+}
 // Resident shapes: first and last radix R0 (a power of two <= 16), one butterfly of those passes
 // per thread, and either a split inner pass or inner radices that are powers of two dividing R0
 // in a palindromic sequence (so that the inverse transform meets the same radices and strides,
@@ -578,6 +586,7 @@ constexpr bool resident_ok() {
   if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % C::PG == 0))
     return false;
   if (has_split_pass<C>()) return C::T >= C::N / R0;
+  if (is_odd_inner_pass<C>(1)) return C::T >= C::N / R0 && (C::N / C::rad[1]) % C::PG == 0;
   for (int p = 0; p < C::NP; ++p) {
     const int r = C::rad[p];
     if (r < 2 || (r & (r - 1)) != 0 || R0 % r != 0 || r != C::rad[C::NP - 1 - p]) return false;
@@ -743,7 +752,8 @@ __device__ __forceinline__ void resident_load(RR& rr, float2* lds, const float2*
     constexpr int OFF = small_tw_offset<C>(P);
     for (int i = t; i < NS * RP; i += C::T) {
       const int jm = i / RP, r = i % RP;
-      if constexpr (is_split_pass<C>(P)) small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
+      if constexpr (is_split_pass<C>(P) || is_odd_inner_pass<C>(P))
+        small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
       else small[OFF + 2 * ((r / 2) * NS + jm) + (r & 1)] = tw[tw_offset<C, false>(P) + i];
     }
   });
@@ -759,6 +769,37 @@ __device__ __forceinline__ float2 twmul(float2 v, float2 t) {
 // Inner pass p (1 <= p <= NP-2) of the resident path: radix R = rad[p], stride NS = the
 // product of the radices before it, LDS -> LDS, twiddles from the LDS copy of the pass-p table;
 // thread t takes butterflies t + T i, i < R0 / R.
+template <class C, int P, bool INV>
+__device__ __forceinline__ void res_odd_pass(float2* __restrict__ lds, int t) {
+  constexpr int R = C::rad[P];
+  constexpr int NB = C::N / R;
+  constexpr int NS = ns_fwd<C>(P);
+  constexpr int BPT = NB / C::T;
+  static_assert(BPT * C::T == NB && NB % C::PG == 0 && pad_offsets_ok<C>(NS, R), "odd inner pass shape");
+  float2 a[BPT][R];
+  sfor<0, BPT>([&](auto iv) {
+    constexpr int i = decltype(iv)::value;
+    const float2* rb = lds + pad<C>(t + C::T * i);
+    sfor<0, R>([&](auto rv) { a[i][decltype(rv)::value] = rb[decltype(rv)::value * pad<C>(NB)]; });
+  });
+  __syncthreads();
+  sfor<0, BPT>([&](auto iv) {
+    constexpr int i = decltype(iv)::value;
+    const int j = t + C::T * i;
+    const int jm = j % NS;
+    const float2* tb = lds + C::LDS + small_tw_offset<C>(P) + jm;  // table [r][jm]
+    auto pre = [&](int r, float2 v) {
+      if (r == 0) return v;
+      const float2 w = tb[r * NS];
+      return INV ? make_float2(v.x * w.x + v.y * w.y, v.y * w.x - v.x * w.y)
+                 : make_float2(v.x * w.x - v.y * w.y, v.x * w.y + v.y * w.x);
+    };
+    float2* wb = lds + pad<C>((j / NS) * NS * R + jm);
+    dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { wb[pad<C>(q * NS)] = v; });
+  });
+  __syncthreads();
+}
+
 template <class C, int P, bool INV>
 __device__ __forceinline__ void res_inner_pass(float2* __restrict__ lds, int t) {
   constexpr int R = C::rad[P];
@@ -893,6 +934,7 @@ __device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
   if constexpr (P >= 1 && P <= C::NP - 2) {
     // the radices are palindromic: the inverse FFT meets the same radices and strides as the forward one
     if constexpr (is_split_pass<C>(P)) split_pass<C, P, INV>(lds, t);
+    else if constexpr (is_odd_inner_pass<C>(P)) res_odd_pass<C, P, INV>(lds, t);
     else res_inner_pass<C, P, INV>(lds, t);
     res_inner_passes<C, P + 1, INV>(lds, t);
   }
