@@ -259,8 +259,15 @@ def test_fp16_input_equals_fp32_of_same_values():
     np.testing.assert_array_equal(a[1].cpu().numpy(), b[1].cpu().numpy())
 
 
-def test_empty_single_and_strided_rows():
-    n, k = 256, 5
+# one length per transform shape: generic (256), lane-paired resident (512, 4096), odd inner pass
+# (768), palindromic resident (1024, 16384), split radix-43 (11008)
+@pytest.mark.parametrize("n", [256, 512, 768, 1024, 4096, 11008, 16384])
+def test_empty_single_and_strided_rows(n):
+    """m = 0 is a no-op; a strided 3-row call (ldw = n + 40) satisfies w = u + P vhat + r with
+    its own residual and matches float64 under the tie-band replay (k = 5 leaves a residual
+    above fp32 resolution, where a sign decision near a tie may go either way, Alg. 2); its
+    unpaired last row equals a 1-row call bit for bit."""
+    k = 5
     plan = K.kashin_plan(n, 1, k)
     rng = np.random.default_rng(5)
     # m = 0: no-op
@@ -270,16 +277,22 @@ def test_empty_single_and_strided_rows():
     wide = _rows(rng, 3, n + 40)
     wv = pu.to_dev(wide)[:, 5:5 + n]
     assert wv.stride(0) == n + 40
-    u, vh, _, _, _ = K.decompose_alloc(plan, wv)
+    u, vh, r, _, _ = K.decompose_alloc(plan, wv, want_r=True)
     u1, vh1, _, _, _ = K.decompose_alloc(plan, pu.to_dev(wide[2:3, 5:5 + n]))
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, wv, [0, 1, 2], k)
     torch.cuda.synchronize()
     eps = ref.sign_mask(n, 1)
     w64 = wide[:, 5:5 + n].astype(np.float64)
-    r_ref = ref.decompose(w64, eps, k)["r"]  # k = 5 leaves a residual above fp32 resolution
-    rec = np.abs(w64 - r_ref - u.cpu().numpy() - ref.apply_p(vh.cpu().numpy().astype(np.float64), eps)).max(1)
-    assert rec.max() <= 1e-5 * np.abs(w64).max()
+    u, vh, r = (t.cpu().numpy().astype(np.float64) for t in (u, vh, r))
+    own = np.abs(w64 - u - ref.apply_p(vh, eps) - r).max() / np.abs(w64).max()
+    res = pu.replay_parity(w64, eps, k, signs, u_tr, v_tr)
+    _say(f"empty/single/strided N={n}: own identity {own:.2e}, replay du={res['du'].max():.2e} "
+         f"in-band flips={res['in_band_flips'].sum()}")
+    assert own <= 1e-5
+    pu.assert_replay_ok(res, f"N={n}")
+    np.testing.assert_array_equal(u_tr, u)  # the trace run is the same computation
     # the unpaired last row of the 3-row call equals the 1-row call bit for bit
-    np.testing.assert_array_equal(u.cpu().numpy()[2], u1.cpu().numpy()[0])
+    np.testing.assert_array_equal(u[2], u1.cpu().numpy()[0].astype(np.float64))
 
 
 def test_unaligned_and_strided_p_map_io():
