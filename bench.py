@@ -3,9 +3,10 @@
 
     python bench.py [--steps K] [--warmup W] [--workload llama7b] [--lloyd 0] [--op quantize]
 
---op quantize (default): one step = kashin_quantize (decompose with Alg. 2 + four-peak 2-bit
-  clustering + packing) over every matrix of the workload (default: one Llama-2-7B-shaped decoder
-  layer, fp16-stored, 30 blocks, closed-form centres), inputs already resident in HBM.
+--op quantize (default): one step = kashin_quantize_grouped (decompose with Alg. 2 + four-peak
+  2-bit clustering + packing) over every matrix of the workload (default: one Llama-2-7B-shaped
+  decoder layer, fp16-stored, 30 blocks, closed-form centres), one launch per vector length and 16
+  matrices (--per-matrix: one kashin_quantize launch per matrix), inputs already resident in HBM.
 --op apply_p: one step = y = P x (kashin_apply_p) over --act-rows fp32 activation rows for each
   input width N of the workload (the inference-side product of App. C).
 --op reconstruct: one step = w_hat = u_q + P v_q (kashin_reconstruct) from the codes and centres
@@ -76,6 +77,10 @@ class Launch:
     nbytes: float         # algorithmic HBM bytes of the launch
     run: Callable         # run(stream)
     kind: str = "quantize"  # which kernel the launch runs: quantize, pmap or rotate
+    wgs: int = 0          # workgroups of the launch's one kernel dispatch (0: one per row pair)
+
+    def workgroups(self) -> int:
+        return self.wgs or (self.rows + 1) // 2
 
 
 def measured_traffic(op: str, workload: str, kernel: str, launches) -> float | None:
@@ -220,6 +225,9 @@ def main() -> int:
     ap.add_argument("--chunk", type=int, default=128, help="columns per compensation chunk (--op optq)")
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
+    ap.add_argument("--per-matrix", action="store_true",
+                    help="--op quantize: one kashin_quantize launch per matrix instead of one "
+                         "kashin_quantize_grouped launch per vector length (up to 16 matrices each)")
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -293,6 +301,8 @@ def main() -> int:
                         spec.rows * hbm_bytes_per_vector(spec.n, 2 if spec.dtype == "f16" else 4),
                         lambda s, a=(plan, wd, cu, cv, ce): K.kashin_quantize_rotated(
                             a[0], ROT_SEED, a[1], args.lloyd, a[2], a[3], a[4], s)))
+                elif args.op == "quantize" and not args.per_matrix:
+                    keep.append((plan, wd, cu, cv, ce))  # grouped by vector length below
                 elif args.op == "quantize":
                     keep.append((plan, wd, cu, cv, ce))
                     launches.append(Launch(
@@ -311,6 +321,19 @@ def main() -> int:
                         spec.rows * (2 * nb + 32 + 4 * spec.n),
                         lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s),
                         kind="pmap"))
+        if args.op == "quantize" and not args.per_matrix:
+            # one grouped launch per vector length and 16 matrices: the row pairs of all of them
+            # share one grid, so no launch ends in a partial wave of workgroups
+            for n in sorted({spec.n for spec in wl.matrices}):
+                items = [it for it in keep if it[0].n == n]
+                for c0 in range(0, len(items), 16):
+                    chunk = items[c0:c0 + 16]
+                    rows = sum(it[1].shape[0] for it in chunk)
+                    in_bytes = chunk[0][1].element_size()
+                    launches.append(Launch(
+                        n, rows, rows * counted_flops_per_vector(n, wl.iters), rows * hbm_bytes_per_vector(n, in_bytes),
+                        lambda s, c=chunk: K.kashin_quantize_grouped(c, args.lloyd, s),
+                        wgs=sum((it[1].shape[0] + 1) // 2 for it in chunk)))
     elif args.op == "optq":
         from paper_2609_11687_amd import optq
 
@@ -409,7 +432,7 @@ def main() -> int:
         roofline = {
             "bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_TFLOPS,
-            "traffic": measured_traffic(args.op, args.workload, kname, [(l.n, (l.rows + 1) // 2) for l, _ in dom]),
+            "traffic": measured_traffic(args.op, args.workload, kname, [(l.n, l.workgroups()) for l, _ in dom]),
             "kernel": f"{kname} N={dom_n}", "launches": len(dom),
             "flops_per_vector": counted_flops_per_vector(dom_n, wl.iters),
             "algorithmic_bytes_per_launch": dom_bytes / len(dom),
@@ -417,7 +440,9 @@ def main() -> int:
         if args.op == "quantize":
             metric, unit = METRIC, "vectors/s"
             workload = (f"{args.workload}: {layer}, {wl.matrices[0].dtype} storage, k={wl.iters} blocks, "
-                        f"lloyd={args.lloyd}, one row = one vector")
+                        f"lloyd={args.lloyd}, one row = one vector, "
+                        + ("one launch per matrix" if args.per_matrix else
+                           "one grouped launch per vector length (kashin_quantize_grouped)"))
         else:
             metric, unit = METRIC_QUANT_H, "vectors/s"
             workload = (f"{args.workload} +H: {layer}, {wl.matrices[0].dtype} rows rotated in the load (R w, seed "

@@ -106,6 +106,28 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
                     int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers,
                     void* stream);
 
+/* One matrix of kashin_quantize_grouped: the arguments kashin_quantize takes for it. */
+typedef struct {
+  kashin_plan_t plan; /* every item's plan has the same n and iters and lives on the same device */
+  const void* w;      /* m rows of n, leading dimension ldw >= n (device) */
+  int64_t m;          /* >= 0; an item with m == 0 is skipped */
+  int64_t ldw;
+  uint8_t* codes_u;   /* m x ceil(n/4) (device) */
+  uint8_t* codes_v;   /* m x ceil(n/4) (device) */
+  float* centers;     /* m x 2 x 4, ascending (device) */
+} kashin_quantize_item;
+
+/* kashin_quantize over several matrices of one vector length, in one launch per 16 matrices: the
+ * quantisation of every matrix of a layer or a model (Sec. 5 applies the method to each weight
+ * matrix, each with its own sign mask, hence its own plan).  The row pairs of all matrices share
+ * one grid, so the chip stays full where a matrix alone would leave a partial last wave of
+ * workgroups.  Every matrix's codes and centres equal those of kashin_quantize on it alone, bit
+ * for bit.  items: host array of `count` entries (count >= 0), read before the call returns; the
+ * per-launch matrix table travels in the kernel arguments (nothing is allocated).  All matrices
+ * share dtype and lloyd_iters.  Output ranges of different items must not overlap. */
+int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, int32_t dtype, int32_t lloyd_iters,
+                            void* stream);
+
 /* y = P x row-wise for fp32 rows (m x n, ld n): the operator of Sec. 4.1 / Alg. 2 alone.
  * x and y may not alias. */
 int kashin_apply_p(kashin_plan_t plan, const float* x, float* y, int64_t m, void* stream);

@@ -277,6 +277,54 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
   return launch(plan, a, (m + 1) / 2, stream);
 }
 
+int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, int32_t dtype, int32_t lloyd_iters,
+                            void* stream) {
+  if (count < 0) return fail(KASHIN_E_INVALID, "count must be >= 0 (got %d)", count);
+  if (count == 0) return ok();
+  if (items == nullptr) return fail(KASHIN_E_INVALID, "items is null");
+  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
+  const kashin_plan_s* p0 = nullptr;
+  for (int32_t i = 0; i < count; ++i) {
+    const kashin_quantize_item& it = items[i];
+    if (!live(it.plan)) return fail(KASHIN_E_INVALID, "item %d: plan is null or destroyed", i);
+    if (p0 == nullptr) {
+      p0 = it.plan;
+    } else if (it.plan->n != p0->n || it.plan->iters != p0->iters || it.plan->device != p0->device) {
+      return fail(KASHIN_E_INVALID, "item %d: plan (n %d, iters %d, device %d) differs from item 0's (n %d, iters %d, "
+                  "device %d)", i, it.plan->n, it.plan->iters, it.plan->device, p0->n, p0->iters, p0->device);
+    }
+    if (it.m < 0) return fail(KASHIN_E_INVALID, "item %d: m must be >= 0 (got %lld)", i, (long long)it.m);
+    if (it.ldw < p0->n) return fail(KASHIN_E_INVALID, "item %d: ldw (%lld) < n (%d)", i, (long long)it.ldw, p0->n);
+    if (it.m > 0 && (!it.w || !it.codes_u || !it.codes_v || !it.centers))
+      return fail(KASHIN_E_INVALID, "item %d: w, codes and centers must be non-null", i);
+  }
+  kashin::KArgs a = base_args(p0, kashin::MODE_QUANTIZE);
+  a.dtype = dtype;
+  a.lloyd = lloyd_iters;
+  int32_t g = 0;
+  int64_t pairs = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const kashin_quantize_item& it = items[i];
+    if (it.m == 0) continue;
+    a.group[g] = kashin::GroupItem{it.plan->d_tw, it.plan->d_mid, it.w, it.ldw, it.m, it.codes_u, it.codes_v,
+                                   it.centers, pairs};
+    pairs += (it.m + 1) / 2;
+    if (++g == kashin::kMaxGroup || i == count - 1) {
+      a.ngroup = g;
+      const int st = launch(p0, a, pairs, stream);
+      if (st) return st;
+      g = 0;
+      pairs = 0;
+    }
+  }
+  if (g > 0) {  // the last items were empty
+    a.ngroup = g;
+    return launch(p0, a, pairs, stream);
+  }
+  return ok();
+}
+
 int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw, const int64_t* rows,
                  int64_t nrows, int8_t* sign_trace, float* c_trace, float* u, float* vhat, void* stream) {
   int st = check_common(plan, m);

@@ -23,6 +23,21 @@ enum Schedule : int32_t {
   SCHED_ORIGINAL = 3,     // Alg. 1: that choice, projection step ||.||_1 / nnz, stop at ||rho|| < tol
 };
 
+// One matrix of a grouped quantisation launch: its plan's tables, rows, outputs, and the index
+// of its first row pair among the launch's workgroups.
+struct GroupItem {
+  const float2* tw;
+  const float4* mid4;
+  const void* w;
+  int64_t ldw;
+  int64_t m;
+  uint8_t* codes_u;
+  uint8_t* codes_v;
+  float* centers;
+  int64_t pair0;
+};
+constexpr int kMaxGroup = 16;  // matrices per grouped launch (the table travels in the kernel arguments)
+
 // Everything a launch needs, passed to the kernel by value.
 struct KArgs {
   // operator tables (plan-owned, device)
@@ -62,6 +77,10 @@ struct KArgs {
   int32_t rot;
   float rot_scale;  // 1 / sqrt(2^a), n = 2^a b
   uint64_t rot_seed;
+  // MODE_QUANTIZE over several matrices of one vector length (ngroup > 0): workgroup p takes
+  // row pair p - group[g].pair0 of the last matrix g with group[g].pair0 <= p
+  int32_t ngroup;
+  GroupItem group[kMaxGroup];
 };
 
 struct ClusterArgs {

@@ -896,21 +896,49 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
     im[decltype(iv)::value] = make_float2(0.f, 0.f);
   });
   float2 sum = x0;
-  sfor<1, H + 1>([&](auto rv) {
-    constexpr int r = decltype(rv)::value;
-    const float2 p = rb[r * pad<C>(NB)], m = rb[(R - r) * pad<C>(NB)];
-    const float2 sp = cadd(p, m), dm = csub(p, m);
-    sum = cadd(sum, sp);
-    const float* cr = cf + (r - 1) * QP * 2;
-    sfor<0, QP>([&](auto iv) {
-      constexpr int i = decltype(iv)::value;
-      const float c = cr[2 * i], sn = cr[2 * i + 1];
-      re[i].x = fmaf(sp.x, c, re[i].x);
-      re[i].y = fmaf(sp.y, c, re[i].y);
-      im[i].x = fmaf(dm.x, sn, im[i].x);
-      im[i].y = fmaf(dm.y, sn, im[i].y);
+  // Input pairs in chunks of CH, software-pipelined: the LDS reads and constant loads of chunk
+  // c + 1 are issued after an explicit wait for those of chunk c, so that the wait (LDS and
+  // scalar loads share one counter, and scalar loads return out of order) never covers loads
+  // that were just issued; chunk c's FMAs then run while chunk c + 1's loads are in flight.
+  constexpr int CH = 1;
+  constexpr int NCH = (H + CH - 1) / CH;
+  float2 pin[2][CH], mnn[2][CH];
+  float cin[2][CH][2 * QP];
+  auto fetch = [&](auto cv) {
+    constexpr int c = decltype(cv)::value;
+    sfor<0, CH>([&](auto uv) {
+      constexpr int u = decltype(uv)::value;
+      constexpr int r = c * CH + u + 1;
+      if constexpr (r <= H) {
+        pin[c % 2][u] = rb[r * pad<C>(NB)];
+        mnn[c % 2][u] = rb[(R - r) * pad<C>(NB)];
+        sfor<0, 2 * QP>([&](auto ev) { cin[c % 2][u][decltype(ev)::value] = cf[(r - 1) * QP * 2 + decltype(ev)::value]; });
+      }
     });
-    if constexpr (r % 2 == 0) __builtin_amdgcn_sched_barrier(0);  // few input pairs in flight
+  };
+  fetch(std::integral_constant<int, 0>{});
+  sfor<0, NCH>([&](auto cv) {
+    constexpr int c = decltype(cv)::value;
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): chunk c's values are in registers
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (c + 1 < NCH) fetch(std::integral_constant<int, c + 1>{});
+    __builtin_amdgcn_sched_barrier(0);
+    sfor<0, CH>([&](auto uv) {
+      constexpr int u = decltype(uv)::value;
+      if constexpr (c * CH + u + 1 <= H) {
+        const float2 p = pin[c % 2][u], m = mnn[c % 2][u];
+        const float2 sp = cadd(p, m), dm = csub(p, m);
+        sum = cadd(sum, sp);
+        sfor<0, QP>([&](auto iv) {
+          constexpr int i = decltype(iv)::value;
+          const float cc = cin[c % 2][u][2 * i], sn = cin[c % 2][u][2 * i + 1];
+          re[i].x = fmaf(sp.x, cc, re[i].x);
+          re[i].y = fmaf(sp.y, cc, re[i].y);
+          im[i].x = fmaf(dm.x, sn, im[i].x);
+          im[i].y = fmaf(dm.y, sn, im[i].y);
+        });
+      }
+    });
   });
   __syncthreads();
   // forward: A_q = re - i im, A_{R-q} = re + i im; the inverse swaps them
@@ -1371,10 +1399,29 @@ __device__ __forceinline__ void store_centers(float* centers, int f, const float
 // Each instance carries only the code and registers of its own variant.
 template <class C, bool LLOYD, bool QUANT, bool ROT>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_greedy_kernel(
-    KArgs a, int64_t item0) {
+    KArgs ka, int64_t item0) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
   __shared__ float red[2 * C::NW * 32];
-  const int64_t item = item0 + blockIdx.x;
+  int64_t item = item0 + blockIdx.x;
+  KArgs a = ka;
+  if constexpr (QUANT) {
+    if (ka.ngroup > 0) {  // grouped launch: the matrix of this row pair (uniform over the workgroup)
+      int gi = 0;
+#pragma unroll
+      for (int g = 1; g < kMaxGroup; ++g)
+        if (g < ka.ngroup && item >= ka.group[g].pair0) gi = g;
+      const GroupItem& it = ka.group[gi];
+      a.tw = it.tw;
+      a.mid4 = it.mid4;
+      a.w = it.w;
+      a.ldw = it.ldw;
+      a.m = it.m;
+      a.codes_u = it.codes_u;
+      a.codes_v = it.codes_v;
+      a.centers = it.centers;
+      item -= it.pair0;
+    }
+  }
   int64_t ra;
   int side = 0;
   if (!QUANT && a.mode == MODE_TRACE) {

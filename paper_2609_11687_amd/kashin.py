@@ -24,7 +24,7 @@ KASHIN_F16 = 1
 EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
-    "kashin_quantize", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
+    "kashin_quantize", "kashin_quantize_grouped", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
     "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_status_string",
     "kashin_last_error",
 )
@@ -59,6 +59,7 @@ def lib() -> ctypes.CDLL:
         "kashin_cluster2bit": [vp, vp, vp, vp, i64, i32, vp, vp, vp, vp],
         "kashin_reconstruct": [vp, vp, vp, vp, i64, vp, i64, vp],
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
+        "kashin_quantize_grouped": [vp, i32, i32, i32, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
         "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
         "kashin_quantize_rotated": [vp, u64, vp, i32, i64, i64, i32, vp, vp, vp, vp],
@@ -108,6 +109,8 @@ def _dtype_code(t) -> int:
 
 def _rows(w):
     """(m, ldw) of a row-major 2-D tensor whose rows are unit-stride."""
+    if w.dim() == 2 and w.shape[0] == 0:  # no rows: strides are arbitrary (torch gives 0 for empty arrays)
+        return 0, w.shape[1]
     if w.dim() != 2 or w.stride(1) != 1:
         raise ValueError("expected a 2-D tensor with unit-stride rows")
     return w.shape[0], w.stride(0)
@@ -194,6 +197,26 @@ def kashin_quantize(plan, w, lloyd_iters, codes_u, codes_v, centers, stream=None
     m, ldw = _rows(w)
     _check(lib().kashin_quantize(plan.handle, _ptr(w), _dtype_code(w), m, ldw, lloyd_iters, _ptr(codes_u),
                                  _ptr(codes_v), _ptr(centers), _stream(stream)))
+
+
+class QuantizeItem(ctypes.Structure):
+    """kashin_quantize_item of include/kashin.h."""
+    _fields_ = [("plan", ctypes.c_void_p), ("w", ctypes.c_void_p), ("m", ctypes.c_int64), ("ldw", ctypes.c_int64),
+                ("codes_u", ctypes.c_void_p), ("codes_v", ctypes.c_void_p), ("centers", ctypes.c_void_p)]
+
+
+def kashin_quantize_grouped(items, lloyd_iters, stream=None):
+    """items: sequence of (plan, w, codes_u, codes_v, centers), one per matrix, all of one dtype."""
+    arr = (QuantizeItem * max(1, len(items)))()
+    dtype = KASHIN_F32
+    for i, (plan, w, cu, cv, ce) in enumerate(items):
+        m, ldw = _rows(w)
+        dtype = _dtype_code(w)
+        arr[i] = QuantizeItem(plan.handle, w.data_ptr(), m, ldw, cu.data_ptr(), cv.data_ptr(), ce.data_ptr())
+    if any(_dtype_code(it[1]) != dtype for it in items):
+        raise TypeError("every matrix of a grouped call has the same dtype")
+    _check(lib().kashin_quantize_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), dtype, lloyd_iters,
+                                         _stream(stream)))
 
 
 def kashin_apply_p(plan, x, y, stream=None):

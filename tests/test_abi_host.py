@@ -141,3 +141,25 @@ def test_rotated_entry_points_reject_dead_plan():
 def test_every_plan_length_is_rotatable(n):
     assert K.kashin_supported_n(n)
     assert n // (n & -n) in (1, 3, 43)
+
+
+def test_grouped_quantize_validation_before_device():
+    """kashin_quantize_grouped checks its item table on the host: an empty table is a no-op, and a
+    null table, a bad count or dtype, or an item with a dead plan is rejected before any launch."""
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1234)
+    buf = 0x1000
+    items = (K.QuantizeItem * 2)()
+    items[0] = K.QuantizeItem(fake, buf, 4, 512, buf, buf, buf)
+    items[1] = K.QuantizeItem(None, buf, 4, 512, buf, buf, buf)
+    table = ctypes.cast(items, ctypes.c_void_p)
+    assert L.kashin_quantize_grouped(table, 0, 0, 0, None) == K.KASHIN_OK
+    assert L.kashin_quantize_grouped(None, 0, 0, 0, None) == K.KASHIN_OK
+    assert L.kashin_quantize_grouped(None, 1, 0, 0, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, -1, 0, 0, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 1, 5, 0, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 1, 0, -1, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 2, 0, 0, None) == K.KASHIN_E_INVALID
+    assert "item 0" in L.kashin_last_error().decode()
+    # the Python binding builds the same table from tensors
+    assert ctypes.sizeof(K.QuantizeItem) == 56

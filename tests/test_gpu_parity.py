@@ -229,6 +229,68 @@ def test_codes_against_oracle_decomposition():
     assert mu + mv <= max(1, int(2e-4 * tot))
 
 
+GROUPED = [  # (n, k, dtype, lloyd, rows per matrix): sizes on every transform shape, empty and
+    # single-row matrices, more matrices than one launch takes
+    (96, 5, torch.float32, 0, [5, 0, 1, 12]),
+    (256, 10, torch.float32, 0, [3, 1, 2, 5, 4, 1, 7, 2, 3, 6, 1, 2, 9, 4, 1, 3, 2, 5, 8]),
+    (512, 20, torch.float32, 2, [7, 4, 0]),
+    (768, 30, torch.float32, 0, [9, 1, 6]),
+    (4096, 30, torch.float16, 0, [6, 0, 3, 10]),
+    (11008, 30, torch.float16, 0, [3, 2, 0, 5]),
+    (16384, 8, torch.float32, 0, [2, 3]),
+]
+
+
+@pytest.mark.parametrize("n,k,dtype,lloyd,rows", GROUPED)
+def test_grouped_quantize_equals_per_matrix(n, k, dtype, lloyd, rows):
+    """kashin_quantize_grouped: every matrix (its own plan and sign mask, one of them strided) gives
+    the codes and centres of kashin_quantize on it alone, bit for bit; one matrix is checked
+    against the oracle's decomposition (tie-band replay) as well."""
+    _say(f"grouped quantize N={n} k={k} rows={rows}")
+    rng = np.random.default_rng(n + 7)
+    items, ref_out, host = [], [], []
+    for i, m in enumerate(rows):
+        w = _rows(rng, m, n, "t4" if i % 2 else "gauss")
+        plan = K.kashin_plan(n, 1000 + 13 * i, k)
+        if i == 1 and m > 0:  # strided rows: ld = n + 8
+            big = torch.zeros((m, n + 8), dtype=dtype, device="cuda")
+            big[:, :n] = pu.to_dev(w, dtype)
+            wd = big[:, :n]
+        else:
+            wd = pu.to_dev(w, dtype)
+        nb = (n + 3) // 4
+        cu = torch.full((m, nb), 0xAB, dtype=torch.uint8, device="cuda")
+        cv = torch.full_like(cu, 0xCD)
+        ce = torch.full((m, 2, 4), float("nan"), dtype=torch.float32, device="cuda")
+        items.append((plan, wd, cu, cv, ce))
+        ref_out.append(K.quantize_alloc(plan, wd, lloyd))
+        host.append(w)
+    K.kashin_quantize_grouped(items, lloyd)
+    torch.cuda.synchronize()
+    for i, ((plan, wd, cu, cv, ce), (cu1, cv1, ce1)) in enumerate(zip(items, ref_out)):
+        assert torch.equal(cu, cu1), f"matrix {i}: codes_u"
+        assert torch.equal(cv, cv1), f"matrix {i}: codes_v"
+        assert torch.equal(ce.view(torch.int32), ce1.view(torch.int32)), f"matrix {i}: centres"
+    # the largest matrix against the oracle
+    i = int(np.argmax(rows))
+    plan, wd, cu, cv, ce = items[i]
+    m = rows[i]
+    eps = ref.sign_mask(n, 1000 + 13 * i)
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, list(range(m)), k)
+    w64 = wd.float().cpu().numpy().astype(np.float64)
+    res = pu.replay_parity(w64, eps, k, signs, u_tr, v_tr)
+    pu.assert_replay_ok(res)
+    if lloyd == 0:
+        rep = res["rep"]
+        qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
+        qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+        pu.assert_centres_close(ce.cpu().numpy()[:, 0], qu)
+        pu.assert_centres_close(ce.cpu().numpy()[:, 1], qv)
+        mu, tot = pu.code_mismatches(pu.unpack(cu.cpu().numpy(), n), rep["u"], qu, res["winf"], "u")
+        mv, _ = pu.code_mismatches(pu.unpack(cv.cpu().numpy(), n), rep["vhat"], qv, res["winf"], "vhat")
+        assert mu + mv <= max(1, int(2e-4 * tot))
+
+
 # ----------------------------------------------------------------------------- properties and edges
 def test_deterministic_and_pow2_homogeneous():
     n, k, m = 512, 20, 6
