@@ -14,7 +14,7 @@ namespace kashin {
   X(768, 64, 3, 16, 3, 16)          \
   X(1024, 64, 2, 16, 4, 16)         \
   X(2048, 128, 2, 16, 8, 16)        \
-  X(3072, 192, 3, 16, 16, 4, 3)     \
+  X(3072, 256, 3, 16, 12, 16)      \
   X(4096, 256, 3, 16, 16, 16)       \
   X(8192, 512, 2, 16, 16, 16, 2)    \
   X(11008, 768, 3, 16, 43, 16)      \

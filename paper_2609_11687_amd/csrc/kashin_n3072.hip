@@ -2,5 +2,5 @@
 #include "kashin_pair_impl.h"
 
 namespace kashin {
-KASHIN_DEFINE_SIZE(3072, 192, 3, 16, 16, 4, 3)
+KASHIN_DEFINE_SIZE(3072, 256, 3, 16, 12, 16)
 }  // namespace kashin

@@ -193,8 +193,8 @@ __device__ __forceinline__ void dft_odd(float2 (&a)[R], Pre&& pre, Sink&& sink) 
     sfor<1, H + 1>([&](auto jv) {
       constexpr int j = decltype(jv)::value;
       constexpr int m = (j * q) % R;
-      constexpr float c = OddTab<R>::c[m];
-      constexpr float sn = OddTab<R>::s[m];
+      constexpr float c = CisTab<R>::c[m];
+      constexpr float sn = CisTab<R>::s[m];
       re.x = fmaf(a[j].x, c, re.x);
       re.y = fmaf(a[j].y, c, re.y);
       im.x = fmaf(a[R - j].x, sn, im.x);
@@ -210,6 +210,60 @@ __device__ __forceinline__ void dft_odd(float2 (&a)[R], Pre&& pre, Sink&& sink) 
     if constexpr (R > 16) __builtin_amdgcn_sched_barrier(0);
   });
   sink(0, sum);
+}
+
+// In-register DFT of an even length R that is not a power of two, from its definition like
+// dft_odd: inputs j and R-j (1 <= j < R/2) are paired into sums and differences, a[0] and
+// a[R/2] enter every output with the signs (+, (-1)^q), and only nonzero constants multiply.
+template <int R, bool INV, class Pre, class Sink>
+__device__ __forceinline__ void dft_even(float2 (&a)[R], Pre&& pre, Sink&& sink) {
+  constexpr int M = R / 2;
+  sfor<1, M>([&](auto jv) {
+    constexpr int j = decltype(jv)::value;
+    const float2 p = pre(j, a[j]), m = pre(R - j, a[R - j]);
+    a[j] = cadd(p, m);
+    a[R - j] = csub(p, m);
+  });
+  const float2 x0 = a[0], xm = pre(M, a[M]);
+  float2 sum = cadd(x0, xm), alt = (M % 2) ? csub(x0, xm) : cadd(x0, xm);  // outputs 0 and M
+  sfor<1, M>([&](auto jv) {
+    constexpr int j = decltype(jv)::value;
+    sum = cadd(sum, a[j]);
+    alt = (j % 2) ? csub(alt, a[j]) : cadd(alt, a[j]);
+  });
+  sfor<1, M>([&](auto qv) {
+    constexpr int q = decltype(qv)::value;
+    float2 re = (q % 2) ? csub(x0, xm) : cadd(x0, xm);
+    float2 im = make_float2(0.f, 0.f);
+    sfor<1, M>([&](auto jv) {
+      constexpr int j = decltype(jv)::value;
+      constexpr int m = (j * q) % R;
+      constexpr float c = CisTab<R>::c[m];
+      constexpr float sn = CisTab<R>::s[m];
+      if constexpr (c != 0.f) {
+        re.x = fmaf(a[j].x, c, re.x);
+        re.y = fmaf(a[j].y, c, re.y);
+      }
+      if constexpr (sn != 0.f) {
+        im.x = fmaf(a[R - j].x, sn, im.x);
+        im.y = fmaf(a[R - j].y, sn, im.y);
+      }
+    });
+    // forward: A_q = re - i im, A_{R-q} = re + i im; inverse swaps them
+    const float2 minus = make_float2(re.x + im.y, re.y - im.x);
+    const float2 plus = make_float2(re.x - im.y, re.y + im.x);
+    sink(q, INV ? plus : minus);
+    sink(R - q, INV ? minus : plus);
+  });
+  sink(0, sum);
+  sink(M, alt);
+}
+
+// DFT of a length R that is not a power of two, outputs handed to sink(q, A_q)
+template <int R, bool INV, class Pre, class Sink>
+__device__ __forceinline__ void dft_small(float2 (&a)[R], Pre&& pre, Sink&& sink) {
+  if constexpr (R % 2 == 1) dft_odd<R, INV>(a, pre, sink);
+  else dft_even<R, INV>(a, pre, sink);
 }
 
 // DFT of a[] handed to sink(q, A_q) for every q (power-of-two R: computed in place first).
@@ -567,13 +621,14 @@ template <class C>
 constexpr bool has_split_pass() {
   return C::NP == 3 && is_split_pass<C>(1);
 }
-// An inner pass of odd radix R < R0 between two radix-R0 passes (N = R0 R R0): its N/R
-// butterflies spread evenly over the T >= N/R0 threads, each read once and transformed by one
-// thread with its twiddles applied to the inputs.
+// An inner pass of a radix R < R0 that is not a power of two (odd, or 12) between two radix-R0
+// passes (N = R0 R R0): its N/R butterflies spread evenly over the T >= N/R0 threads, each read
+// once and transformed by one thread with its twiddles applied to the inputs.
 template <class C>
-constexpr bool is_odd_inner_pass(int p) {
+constexpr bool is_small_inner_pass(int p) {
   const int R = C::rad[p];
-  return C::NP == 3 && p == 1 && R % 2 == 1 && R < C::R0 && C::T % 64 == 0 && (C::N / R) % C::T == 0;
+  return C::NP == 3 && p == 1 && (R & (R - 1)) != 0 && (R % 2 == 1 || R == 12) && R < C::R0 && C::T % 64 == 0 &&
+         (C::N / R) % C::T == 0;
 }
 // Resident shapes: first and last radix R0 (a power of two <= 16), one butterfly of those passes
 // per thread, and either a split inner pass or inner radices that are powers of two dividing R0
@@ -586,7 +641,7 @@ constexpr bool resident_ok() {
   if (!(C::NP >= 2 && R0 <= 16 && (R0 & (R0 - 1)) == 0 && C::rad[C::NP - 1] == R0 && (C::N / R0) % C::PG == 0))
     return false;
   if (has_split_pass<C>()) return C::T >= C::N / R0;
-  if (is_odd_inner_pass<C>(1)) return C::T >= C::N / R0 && (C::N / C::rad[1]) % C::PG == 0;
+  if (is_small_inner_pass<C>(1)) return C::T >= C::N / R0 && (C::N / C::rad[1]) % C::PG == 0;
   for (int p = 0; p < C::NP; ++p) {
     const int r = C::rad[p];
     if (r < 2 || (r & (r - 1)) != 0 || R0 % r != 0 || r != C::rad[C::NP - 1 - p]) return false;
@@ -752,7 +807,7 @@ __device__ __forceinline__ void resident_load(RR& rr, float2* lds, const float2*
     constexpr int OFF = small_tw_offset<C>(P);
     for (int i = t; i < NS * RP; i += C::T) {
       const int jm = i / RP, r = i % RP;
-      if constexpr (is_split_pass<C>(P) || is_odd_inner_pass<C>(P))
+      if constexpr (is_split_pass<C>(P) || is_small_inner_pass<C>(P))
         small[OFF + r * NS + jm] = tw[tw_offset<C, false>(P) + i];
       else small[OFF + 2 * ((r / 2) * NS + jm) + (r & 1)] = tw[tw_offset<C, false>(P) + i];
     }
@@ -770,12 +825,12 @@ __device__ __forceinline__ float2 twmul(float2 v, float2 t) {
 // product of the radices before it, LDS -> LDS, twiddles from the LDS copy of the pass-p table;
 // thread t takes butterflies t + T i, i < R0 / R.
 template <class C, int P, bool INV>
-__device__ __forceinline__ void res_odd_pass(float2* __restrict__ lds, int t) {
+__device__ __forceinline__ void res_small_pass(float2* __restrict__ lds, int t) {
   constexpr int R = C::rad[P];
   constexpr int NB = C::N / R;
   constexpr int NS = ns_fwd<C>(P);
   constexpr int BPT = NB / C::T;
-  static_assert(BPT * C::T == NB && NB % C::PG == 0 && pad_offsets_ok<C>(NS, R), "odd inner pass shape");
+  static_assert(BPT * C::T == NB && NB % C::PG == 0 && pad_offsets_ok<C>(NS, R), "small inner pass shape");
   float2 a[BPT][R];
   sfor<0, BPT>([&](auto iv) {
     constexpr int i = decltype(iv)::value;
@@ -795,7 +850,7 @@ __device__ __forceinline__ void res_odd_pass(float2* __restrict__ lds, int t) {
                  : make_float2(v.x * w.x - v.y * w.y, v.x * w.y + v.y * w.x);
     };
     float2* wb = lds + pad<C>((j / NS) * NS * R + jm);
-    dft_odd<R, INV>(a[i], pre, [&](int q, float2 v) { wb[pad<C>(q * NS)] = v; });
+    dft_small<R, INV>(a[i], pre, [&](int q, float2 v) { wb[pad<C>(q * NS)] = v; });
   });
   __syncthreads();
 }
@@ -866,8 +921,8 @@ constexpr SplitCoef<R, S> make_split_coef() {
         const int q = s * QP + 1 + i;
         const int idx = ((s * H + r - 1) * QP + i) * 2;
         if (q <= H) {
-          t.v[idx] = OddTab<R>::c[(r * q) % R];
-          t.v[idx + 1] = OddTab<R>::s[(r * q) % R];
+          t.v[idx] = CisTab<R>::c[(r * q) % R];
+          t.v[idx + 1] = CisTab<R>::s[(r * q) % R];
         }
       }
   return t;
@@ -962,7 +1017,7 @@ __device__ __forceinline__ void res_inner_passes(float2* lds, int t) {
   if constexpr (P >= 1 && P <= C::NP - 2) {
     // the radices are palindromic: the inverse FFT meets the same radices and strides as the forward one
     if constexpr (is_split_pass<C>(P)) split_pass<C, P, INV>(lds, t);
-    else if constexpr (is_odd_inner_pass<C>(P)) res_odd_pass<C, P, INV>(lds, t);
+    else if constexpr (is_small_inner_pass<C>(P)) res_small_pass<C, P, INV>(lds, t);
     else res_inner_pass<C, P, INV>(lds, t);
     res_inner_passes<C, P + 1, INV>(lds, t);
   }

@@ -235,6 +235,7 @@ GROUPED = [  # (n, k, dtype, lloyd, rows per matrix): sizes on every transform s
     (256, 10, torch.float32, 0, [3, 1, 2, 5, 4, 1, 7, 2, 3, 6, 1, 2, 9, 4, 1, 3, 2, 5, 8]),
     (512, 20, torch.float32, 2, [7, 4, 0]),
     (768, 30, torch.float32, 0, [9, 1, 6]),
+    (3072, 30, torch.float32, 0, [4, 7]),
     (4096, 30, torch.float16, 0, [6, 0, 3, 10]),
     (11008, 30, torch.float16, 0, [3, 2, 0, 5]),
     (16384, 8, torch.float32, 0, [2, 3]),
@@ -323,7 +324,7 @@ def test_fp16_input_equals_fp32_of_same_values():
 
 # one length per transform shape: generic (256), lane-paired resident (512, 4096), odd inner pass
 # (768), palindromic resident (1024, 16384), split radix-43 (11008)
-@pytest.mark.parametrize("n", [256, 512, 768, 1024, 4096, 11008, 16384])
+@pytest.mark.parametrize("n", [256, 512, 768, 1024, 3072, 4096, 11008, 16384])
 def test_empty_single_and_strided_rows(n):
     """m = 0 is a no-op; a strided 3-row call (ldw = n + 40) satisfies w = u + P vhat + r with
     its own residual and matches float64 under the tie-band replay (k = 5 leaves a residual
@@ -432,17 +433,27 @@ def _sample_rows(w, count, rng):
 WL = [("gauss512", None), ("opt125m", 4), ("llama7b", 3), ("pythia7b", 2)]
 
 
-def _check_matrix(key, wl, layer, idx, per_matrix, rng):
-    """Quantise matrix idx of layer `layer` in full (the launch configuration the benchmark
-    times), replay sampled rows (all rows if per_matrix is None) against the oracle: factors,
-    reconstruction, centres and codes.  Returns (code mismatches, codes compared)."""
+def _load_matrix(wl, layer, idx):
+    """(host rows, device rows, plan, (codes_u, codes_v, centres) buffers) of one matrix."""
     spec = wl.matrices[idx]
     w = synth.make_matrix(wl, layer, idx)
-    seed = synth.sign_seed(wl, layer, idx)
-    plan = K.kashin_plan(spec.n, seed, wl.iters)
+    plan = K.kashin_plan(spec.n, synth.sign_seed(wl, layer, idx), wl.iters)
     dt = torch.float16 if spec.dtype == "f16" else torch.float32
     wd = pu.to_dev(w).to(dt)
-    cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+    nb = (spec.n + 3) // 4
+    out = (torch.empty((spec.rows, nb), dtype=torch.uint8, device="cuda"),
+           torch.empty((spec.rows, nb), dtype=torch.uint8, device="cuda"),
+           torch.empty((spec.rows, 2, 4), dtype=torch.float32, device="cuda"))
+    return w, wd, plan, out
+
+
+def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded):
+    """Replay sampled rows (all rows if per_matrix is None) of matrix idx, already quantised in
+    full in the benchmark's launch configuration, against the oracle: factors, reconstruction,
+    centres and codes.  Returns (code mismatches, codes compared)."""
+    spec = wl.matrices[idx]
+    w, wd, plan, (cu, cv, ce) = loaded
+    seed = synth.sign_seed(wl, layer, idx)
     rows = list(range(w.shape[0])) if per_matrix is None else _sample_rows(w, per_matrix, rng)
     signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, rows, wl.iters)
     eps = ref.sign_mask(spec.n, seed)
@@ -463,22 +474,36 @@ def _check_matrix(key, wl, layer, idx, per_matrix, rng):
     mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat")
     # every row of the matrix got finite centres
     assert np.isfinite(ce.cpu().numpy()).all()
-    del plan
     return mu + mv, 2 * tot
+
+
+def _quantize_grouped(loaded):
+    """One kashin_quantize_grouped call per vector length (at most 16 matrices each), as the
+    benchmark launches them."""
+    by_n = {}
+    for w, wd, plan, out in loaded:
+        by_n.setdefault(plan.n, []).append((plan, wd) + out)
+    for items in by_n.values():
+        for c0 in range(0, len(items), 16):
+            K.kashin_quantize_grouped(items[c0:c0 + 16], 0)
+    torch.cuda.synchronize()
 
 
 @pytest.mark.parametrize("key,per_matrix", WL)
 def test_workload_sampled_rows(key, per_matrix):
-    """Every matrix of the workload (first layer) quantised in full; sampled rows replayed."""
+    """Every matrix of the workload (first layer) quantised in full by the grouped launches the
+    benchmark times; sampled rows replayed."""
     wl = synth.WORKLOADS[key]
     rng = np.random.default_rng(11)
+    loaded = [_load_matrix(wl, 0, idx) for idx in range(len(wl.matrices))]
+    _quantize_grouped(loaded)
     total_m = total_codes = 0
     for idx, spec in enumerate(wl.matrices):
         if key == "llama7b" and spec.name in ("k_proj", "v_proj", "up_proj"):
             continue  # same shapes as q_proj / gate_proj; keeps the test within its time budget
         if key == "pythia7b" and spec.name in ("qkv_1", "qkv_2", "dense"):
             continue
-        mm, tot = _check_matrix(key, wl, 0, idx, per_matrix, rng)
+        mm, tot = _check_matrix(key, wl, 0, idx, per_matrix, rng, loaded[idx])
         total_m += mm
         total_codes += tot
     _say(f"{key}: code mismatches {total_m} of {total_codes}")
@@ -494,7 +519,9 @@ def test_stack_first_and_last_layer():
     total_m = total_codes = 0
     for layer in (0, wl.layers - 1):
         for name in ("q_proj", "down_proj"):
-            mm, tot = _check_matrix("llama7b_stack", wl, layer, names.index(name), 2, rng)
+            loaded = _load_matrix(wl, layer, names.index(name))
+            _quantize_grouped([loaded])
+            mm, tot = _check_matrix("llama7b_stack", wl, layer, names.index(name), 2, rng, loaded)
             total_m += mm
             total_codes += tot
     _say(f"llama7b_stack: code mismatches {total_m} of {total_codes}")
