@@ -656,9 +656,11 @@ constexpr int small_tw_offset(int p) {
   for (int q = 1; q < p; ++q) off += ns_fwd<C>(q) * C::rad[q];
   return off;
 }
+// LDS after the FFT buffer on the resident path: the inner-pass twiddle tables, then (with a
+// split pass) the 256-byte lane order of its butterflies
 template <class C>
 constexpr int small_tw_total() {
-  return resident_ok<C>() ? small_tw_offset<C>(C::NP - 1) : 0;
+  return resident_ok<C>() ? small_tw_offset<C>(C::NP - 1) + (has_split_pass<C>() ? 32 : 0) : 0;
 }
 
 // eps factors f_k of the fused step for the thread's elements k = t + q N/R: kept as R complex
@@ -812,6 +814,11 @@ __device__ __forceinline__ void resident_load(RR& rr, float2* lds, const float2*
       else small[OFF + 2 * ((r / 2) * NS + jm) + (r & 1)] = tw[tw_offset<C, false>(P) + i];
     }
   });
+  if constexpr (has_split_pass<C>()) {
+    const unsigned char* order = SplitOrder<C::rad[1]>::j;
+    unsigned char* dst = reinterpret_cast<unsigned char*>(small + small_tw_offset<C>(C::NP - 1));
+    for (int i = threadIdx.x; i < 256; i += C::T) dst[i] = order[i];
+  }
   __syncthreads();
 }
 
@@ -941,7 +948,10 @@ __device__ __forceinline__ void split_pass(float2* __restrict__ lds, int t) {
   constexpr int NS = ns_fwd<C>(P);
   static_assert(NB % 64 == 0 && NS % C::PG == 0, "split pass strides");
   const int s = __builtin_amdgcn_readfirstlane(t / NB);  // uniform across a wave
-  const int j = t - s * NB;
+  // butterfly of this lane: the order of SplitOrder (bank-conflict-free reads in seven of the
+  // eight 32-lane halves, conflict-free writes), kept in LDS after the twiddle tables
+  static_assert(NB == 256, "split-pass lane order covers 256 butterflies");
+  const int j = reinterpret_cast<const unsigned char*>(lds + C::LDS + small_tw_offset<C>(C::NP - 1))[t - s * NB];
   const float* __restrict__ cf = split_coef<R, S>.v + s * (H * QP * 2);
   const float2* rb = lds + pad<C>(j);
   const float2 x0 = rb[0];
