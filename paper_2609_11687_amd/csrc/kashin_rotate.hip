@@ -21,6 +21,7 @@ namespace {
 
 constexpr int kRotThreads = 256;
 constexpr int kRotMaxN = 16384;
+constexpr int kBatch = 16;  // row elements per thread loaded together
 
 __device__ __forceinline__ float load_f32(const float* p) { return *p; }
 __device__ __forceinline__ float load_f32(const __half* p) { return __half2float(*p); }
@@ -31,9 +32,20 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t see
   extern __shared__ float buf[];  // n floats
   const int64_t row = row0 + blockIdx.x;
   const IT* xr = x + row * ldx;
-  for (int i = threadIdx.x; i < n; i += kRotThreads) {
-    const float v = load_f32(xr + i);
-    buf[i] = INV ? v : v * rot_sign(seed, i);
+  // loads in batches of kBatch per thread, all issued before the first is used, so a row's
+  // load is one memory latency per batch rather than one per element
+  for (int i0 = threadIdx.x; i0 < n; i0 += kRotThreads * kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int i = i0 + k * kRotThreads;
+      v[k] = load_f32(xr + (i < n ? i : n - 1));  // unconditional (an in-row index), so all loads issue together
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int i = i0 + k * kRotThreads;
+      if (i < n) buf[i] = INV ? v[k] : v[k] * rot_sign(seed, i);
+    }
   }
   __syncthreads();
   const int tid = threadIdx.x;
