@@ -13,8 +13,8 @@
   of every matrix of the workload (quantized once, untimed).
 --op rotate: one step = the incoherence pre-rotation R w (kashin_rotate) of every matrix of the
   workload, fp16 rows in, fp32 rows out.
---op quantize_h: one step = the "+H" pipeline, kashin_quantize_rotated (R w formed in the load,
-  then quantised) over every matrix of the workload.
+--op quantize_h: one step = the "+H" pipeline, R w formed in the load, then quantised
+  (kashin_quantize_grouped with a rotation seed; --per-matrix: kashin_quantize_rotated per matrix).
 --op schedule: one step = kashin_decompose_schedule (--schedule alternating | reverse | adaptive |
   original) over every matrix of the workload, 4k atomic steps, factors and residual written.
 --op optq: one step = the chunked error-compensated pipeline (paper_2609_11687_amd.optq) on one
@@ -226,8 +226,8 @@ def main() -> int:
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--per-matrix", action="store_true",
-                    help="--op quantize: one kashin_quantize launch per matrix instead of one "
-                         "kashin_quantize_grouped launch per vector length (up to 16 matrices each)")
+                    help="--op quantize / quantize_h: one kashin_quantize(_rotated) launch per matrix instead "
+                         "of one kashin_quantize_grouped launch per vector length (up to 16 matrices each)")
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -294,6 +294,8 @@ def main() -> int:
                         spec.rows * spec.n * (2 + 4),
                         lambda s, a=(spec.n, wd, wr): K.kashin_rotate(a[0], ROT_SEED, a[1], a[2], stream=s),
                         kind="rotate"))
+                elif args.op == "quantize_h" and not args.per_matrix:
+                    keep.append((plan, wd, cu, cv, ce))  # grouped by vector length below
                 elif args.op == "quantize_h":
                     keep.append((plan, wd, cu, cv, ce))
                     launches.append(Launch(
@@ -321,7 +323,7 @@ def main() -> int:
                         spec.rows * (2 * nb + 32 + 4 * spec.n),
                         lambda s, a=(plan, cu, cv, ce, wh): K.kashin_reconstruct(a[0], a[1], a[2], a[3], a[4], s),
                         kind="pmap"))
-        if args.op == "quantize" and not args.per_matrix:
+        if args.op in ("quantize", "quantize_h") and not args.per_matrix:
             # one grouped launch per vector length and 16 matrices: the row pairs of all of them
             # share one grid, so no launch ends in a partial wave of workgroups
             for n in sorted({spec.n for spec in wl.matrices}):
@@ -332,7 +334,8 @@ def main() -> int:
                     in_bytes = chunk[0][1].element_size()
                     launches.append(Launch(
                         n, rows, rows * counted_flops_per_vector(n, wl.iters), rows * hbm_bytes_per_vector(n, in_bytes),
-                        lambda s, c=chunk: K.kashin_quantize_grouped(c, args.lloyd, s),
+                        lambda s, c=chunk: K.kashin_quantize_grouped(
+                            c, args.lloyd, s, rot_seed=ROT_SEED if args.op == "quantize_h" else None),
                         wgs=sum((it[1].shape[0] + 1) // 2 for it in chunk)))
     elif args.op == "optq":
         from paper_2609_11687_amd import optq
@@ -446,7 +449,9 @@ def main() -> int:
         else:
             metric, unit = METRIC_QUANT_H, "vectors/s"
             workload = (f"{args.workload} +H: {layer}, {wl.matrices[0].dtype} rows rotated in the load (R w, seed "
-                        f"{ROT_SEED}) and quantised, k={wl.iters} blocks, lloyd={args.lloyd}")
+                        f"{ROT_SEED}) and quantised, k={wl.iters} blocks, lloyd={args.lloyd}, "
+                        + ("one launch per matrix" if args.per_matrix else
+                           "one grouped launch per vector length (kashin_quantize_grouped)"))
     else:
         achieved = dom_bytes / dom_s / 1e9
         kname = f"rotate_kernel[b={dom_n // (dom_n & -dom_n)}]" if main_kind == "rotate" else "pair_pmap_kernel"

@@ -121,12 +121,13 @@ typedef struct {
  * quantisation of every matrix of a layer or a model (Sec. 5 applies the method to each weight
  * matrix, each with its own sign mask, hence its own plan).  The row pairs of all matrices share
  * one grid, so the chip stays full where a matrix alone would leave a partial last wave of
- * workgroups.  Every matrix's codes and centres equal those of kashin_quantize on it alone, bit
- * for bit.  items: host array of `count` entries (count >= 0), read before the call returns; the
- * per-launch matrix table travels in the kernel arguments (nothing is allocated).  All matrices
- * share dtype and lloyd_iters.  Output ranges of different items must not overlap. */
+ * workgroups.  Every matrix's codes and centres equal those of kashin_quantize on it alone (or,
+ * with rot_seed non-NULL, of kashin_quantize_rotated with seed *rot_seed), bit for bit.
+ * items: host array of `count` entries (count >= 0), read before the call returns; the per-launch
+ * matrix table travels in the kernel arguments (nothing is allocated).  All matrices share dtype,
+ * lloyd_iters and the rotation.  Output ranges of different items must not overlap. */
 int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, int32_t dtype, int32_t lloyd_iters,
-                            void* stream);
+                            const uint64_t* rot_seed, void* stream);
 
 /* y = P x row-wise for fp32 rows (m x n, ld n): the operator of Sec. 4.1 / Alg. 2 alone.
  * x and y may not alias. */

@@ -278,7 +278,7 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
 }
 
 int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, int32_t dtype, int32_t lloyd_iters,
-                            void* stream) {
+                            const uint64_t* rot_seed, void* stream) {
   if (count < 0) return fail(KASHIN_E_INVALID, "count must be >= 0 (got %d)", count);
   if (count == 0) return ok();
   if (items == nullptr) return fail(KASHIN_E_INVALID, "items is null");
@@ -302,6 +302,7 @@ int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, in
   kashin::KArgs a = base_args(p0, kashin::MODE_QUANTIZE);
   a.dtype = dtype;
   a.lloyd = lloyd_iters;
+  if (rot_seed != nullptr) set_rotation(&a, p0->n, *rot_seed);
   int32_t g = 0;
   int64_t pairs = 0;
   for (int32_t i = 0; i < count; ++i) {

@@ -59,7 +59,7 @@ def lib() -> ctypes.CDLL:
         "kashin_cluster2bit": [vp, vp, vp, vp, i64, i32, vp, vp, vp, vp],
         "kashin_reconstruct": [vp, vp, vp, vp, i64, vp, i64, vp],
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
-        "kashin_quantize_grouped": [vp, i32, i32, i32, vp],
+        "kashin_quantize_grouped": [vp, i32, i32, i32, vp, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
         "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
         "kashin_quantize_rotated": [vp, u64, vp, i32, i64, i64, i32, vp, vp, vp, vp],
@@ -205,8 +205,9 @@ class QuantizeItem(ctypes.Structure):
                 ("codes_u", ctypes.c_void_p), ("codes_v", ctypes.c_void_p), ("centers", ctypes.c_void_p)]
 
 
-def kashin_quantize_grouped(items, lloyd_iters, stream=None):
-    """items: sequence of (plan, w, codes_u, codes_v, centers), one per matrix, all of one dtype."""
+def kashin_quantize_grouped(items, lloyd_iters, stream=None, rot_seed=None):
+    """items: sequence of (plan, w, codes_u, codes_v, centers), one per matrix, all of one dtype;
+    rot_seed: None, or the seed of the incoherence rotation applied to every matrix's rows."""
     arr = (QuantizeItem * max(1, len(items)))()
     dtype = KASHIN_F32
     for i, (plan, w, cu, cv, ce) in enumerate(items):
@@ -215,7 +216,8 @@ def kashin_quantize_grouped(items, lloyd_iters, stream=None):
         arr[i] = QuantizeItem(plan.handle, w.data_ptr(), m, ldw, cu.data_ptr(), cv.data_ptr(), ce.data_ptr())
     if any(_dtype_code(it[1]) != dtype for it in items):
         raise TypeError("every matrix of a grouped call has the same dtype")
-    _check(lib().kashin_quantize_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), dtype, lloyd_iters,
+    seed = None if rot_seed is None else ctypes.byref(ctypes.c_uint64(rot_seed))
+    _check(lib().kashin_quantize_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), dtype, lloyd_iters, seed,
                                          _stream(stream)))
 
 

@@ -153,13 +153,13 @@ def test_grouped_quantize_validation_before_device():
     items[0] = K.QuantizeItem(fake, buf, 4, 512, buf, buf, buf)
     items[1] = K.QuantizeItem(None, buf, 4, 512, buf, buf, buf)
     table = ctypes.cast(items, ctypes.c_void_p)
-    assert L.kashin_quantize_grouped(table, 0, 0, 0, None) == K.KASHIN_OK
-    assert L.kashin_quantize_grouped(None, 0, 0, 0, None) == K.KASHIN_OK
-    assert L.kashin_quantize_grouped(None, 1, 0, 0, None) == K.KASHIN_E_INVALID
-    assert L.kashin_quantize_grouped(table, -1, 0, 0, None) == K.KASHIN_E_INVALID
-    assert L.kashin_quantize_grouped(table, 1, 5, 0, None) == K.KASHIN_E_INVALID
-    assert L.kashin_quantize_grouped(table, 1, 0, -1, None) == K.KASHIN_E_INVALID
-    assert L.kashin_quantize_grouped(table, 2, 0, 0, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 0, 0, 0, None, None) == K.KASHIN_OK
+    assert L.kashin_quantize_grouped(None, 0, 0, 0, None, None) == K.KASHIN_OK
+    assert L.kashin_quantize_grouped(None, 1, 0, 0, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, -1, 0, 0, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 1, 5, 0, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 1, 0, -1, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_quantize_grouped(table, 2, 0, 0, None, None) == K.KASHIN_E_INVALID
     assert "item 0" in L.kashin_last_error().decode()
     # the Python binding builds the same table from tensors
     assert ctypes.sizeof(K.QuantizeItem) == 56

@@ -229,25 +229,29 @@ def test_codes_against_oracle_decomposition():
     assert mu + mv <= max(1, int(2e-4 * tot))
 
 
-GROUPED = [  # (n, k, dtype, lloyd, rows per matrix): sizes on every transform shape, empty and
-    # single-row matrices, more matrices than one launch takes
-    (96, 5, torch.float32, 0, [5, 0, 1, 12]),
-    (256, 10, torch.float32, 0, [3, 1, 2, 5, 4, 1, 7, 2, 3, 6, 1, 2, 9, 4, 1, 3, 2, 5, 8]),
-    (512, 20, torch.float32, 2, [7, 4, 0]),
-    (768, 30, torch.float32, 0, [9, 1, 6]),
-    (3072, 30, torch.float32, 0, [4, 7]),
-    (4096, 30, torch.float16, 0, [6, 0, 3, 10]),
-    (11008, 30, torch.float16, 0, [3, 2, 0, 5]),
-    (16384, 8, torch.float32, 0, [2, 3]),
+GROUPED = [  # (n, k, dtype, lloyd, rows per matrix, rotation seed): sizes on every transform shape,
+    # empty and single-row matrices, more matrices than one launch takes, the fused rotation
+    (96, 5, torch.float32, 0, [5, 0, 1, 12], None),
+    (256, 10, torch.float32, 0, [3, 1, 2, 5, 4, 1, 7, 2, 3, 6, 1, 2, 9, 4, 1, 3, 2, 5, 8], None),
+    (512, 20, torch.float32, 2, [7, 4, 0], None),
+    (768, 30, torch.float32, 0, [9, 1, 6], None),
+    (3072, 30, torch.float32, 0, [4, 7], None),
+    (4096, 30, torch.float16, 0, [6, 0, 3, 10], None),
+    (11008, 30, torch.float16, 0, [3, 2, 0, 5], None),
+    (16384, 8, torch.float32, 0, [2, 3], None),
+    (768, 30, torch.float32, 0, [5, 4], 99),
+    (4096, 30, torch.float16, 0, [6, 3, 1], 99),
+    (11008, 30, torch.float16, 0, [3, 4], 99),
 ]
 
 
-@pytest.mark.parametrize("n,k,dtype,lloyd,rows", GROUPED)
-def test_grouped_quantize_equals_per_matrix(n, k, dtype, lloyd, rows):
+@pytest.mark.parametrize("n,k,dtype,lloyd,rows,rot", GROUPED)
+def test_grouped_quantize_equals_per_matrix(n, k, dtype, lloyd, rows, rot):
     """kashin_quantize_grouped: every matrix (its own plan and sign mask, one of them strided) gives
-    the codes and centres of kashin_quantize on it alone, bit for bit; one matrix is checked
-    against the oracle's decomposition (tie-band replay) as well."""
-    _say(f"grouped quantize N={n} k={k} rows={rows}")
+    the codes and centres of kashin_quantize (kashin_quantize_rotated with a rotation seed) on it
+    alone, bit for bit; without rotation one matrix is checked against the oracle's decomposition
+    (tie-band replay) as well."""
+    _say(f"grouped quantize N={n} k={k} rows={rows} rotation={rot}")
     rng = np.random.default_rng(n + 7)
     items, ref_out, host = [], [], []
     for i, m in enumerate(rows):
@@ -264,14 +268,21 @@ def test_grouped_quantize_equals_per_matrix(n, k, dtype, lloyd, rows):
         cv = torch.full_like(cu, 0xCD)
         ce = torch.full((m, 2, 4), float("nan"), dtype=torch.float32, device="cuda")
         items.append((plan, wd, cu, cv, ce))
-        ref_out.append(K.quantize_alloc(plan, wd, lloyd))
+        if rot is None:
+            ref_out.append(K.quantize_alloc(plan, wd, lloyd))
+        else:
+            r1 = (torch.empty_like(cu), torch.empty_like(cv), torch.empty_like(ce))
+            K.kashin_quantize_rotated(plan, rot, wd, lloyd, *r1)
+            ref_out.append(r1)
         host.append(w)
-    K.kashin_quantize_grouped(items, lloyd)
+    K.kashin_quantize_grouped(items, lloyd, rot_seed=rot)
     torch.cuda.synchronize()
     for i, ((plan, wd, cu, cv, ce), (cu1, cv1, ce1)) in enumerate(zip(items, ref_out)):
         assert torch.equal(cu, cu1), f"matrix {i}: codes_u"
         assert torch.equal(cv, cv1), f"matrix {i}: codes_v"
         assert torch.equal(ce.view(torch.int32), ce1.view(torch.int32)), f"matrix {i}: centres"
+    if rot is not None:
+        return  # the rotated path alone is checked against the oracle by the rotation tests
     # the largest matrix against the oracle
     i = int(np.argmax(rows))
     plan, wd, cu, cv, ce = items[i]
