@@ -108,19 +108,31 @@ __device__ __forceinline__ void rot_odd_factor_fixed(V* buf, int tid) {
   }
 }
 
+// Slot of entry e of a row held in LDS: e, or with PAD (B = 1 only) e + e/16, one spare word per
+// 16 entries, so that the 16 consecutive entries a thread of the first Hadamard pass takes, the
+// stride-16 groups of the second and the row-order loads and stores all spread over the banks.
+template <bool PAD>
+__device__ __forceinline__ int rot_slot(int e) {
+  return PAD ? e + (e >> 4) : e;
+}
+
 // One pass of the unnormalised Walsh-Hadamard transform over the segment-index bits
 // [lh, lh + log2 R): each thread takes groups of R entries at stride 2^lh B, transforms them in
 // registers with radix-2 stages in ascending bit order, and writes them back; then a barrier.
 // Consecutive threads take consecutive offsets within a stride, so each access is contiguous.
-template <int B, int R, int T, class V>
+// With PAD the entries sit at rot_slot<true> (the stride 2^lh is then 1 or a multiple of 16, so
+// entries hb apart are hb + hb/16 slots apart).
+template <int B, int R, int T, bool PAD = false, class V>
 __device__ __forceinline__ void rot_hadamard_pass(V* buf, int n, int lh, int tid) {
+  static_assert(!PAD || B == 1, "padded rows are power-of-two rows");
   const int hb = (1 << lh) * B;
+  const int st = PAD ? hb + (hb >> 4) : hb;
   for (int q = tid; q < n / R; q += T) {
     const int hi = (q >> lh) / B;  // = q / hb
-    V* p = buf + hi * (R * hb) + (q - hi * hb);
+    V* p = buf + rot_slot<PAD>(hi * (R * hb) + (q - hi * hb));
     V x[R];
 #pragma unroll
-    for (int m = 0; m < R; ++m) x[m] = p[m * hb];
+    for (int m = 0; m < R; ++m) x[m] = p[m * st];
 #pragma unroll
     for (int st = 1; st < R; st <<= 1) {
 #pragma unroll
@@ -133,22 +145,22 @@ __device__ __forceinline__ void rot_hadamard_pass(V* buf, int n, int lh, int tid
       }
     }
 #pragma unroll
-    for (int m = 0; m < R; ++m) p[m * hb] = x[m];
+    for (int m = 0; m < R; ++m) p[m * st] = x[m];
   }
   __syncthreads();
 }
 
 // unnormalised Walsh-Hadamard transform over the 2^a segments (stride B), in place: passes of
 // radix 16 (a last one of radix 2, 4 or 8), the radix-2 stages in ascending bit order overall
-template <int B, int T, class V>
+template <int B, int T, bool PAD = false, class V>
 __device__ __forceinline__ void rot_hadamard(V* buf, int n, int tid) {
   const int a = __builtin_ctz(static_cast<unsigned>(n));  // n = 2^a B, B odd
   int lh = 0;
-  for (; lh + 4 <= a; lh += 4) rot_hadamard_pass<B, 16, T>(buf, n, lh, tid);
+  for (; lh + 4 <= a; lh += 4) rot_hadamard_pass<B, 16, T, PAD>(buf, n, lh, tid);
   const int r = a - lh;
-  if (r == 3) rot_hadamard_pass<B, 8, T>(buf, n, lh, tid);
-  else if (r == 2) rot_hadamard_pass<B, 4, T>(buf, n, lh, tid);
-  else if (r == 1) rot_hadamard_pass<B, 2, T>(buf, n, lh, tid);
+  if (r == 3) rot_hadamard_pass<B, 8, T, PAD>(buf, n, lh, tid);
+  else if (r == 2) rot_hadamard_pass<B, 4, T, PAD>(buf, n, lh, tid);
+  else if (r == 1) rot_hadamard_pass<B, 2, T, PAD>(buf, n, lh, tid);
 }
 
 // b, the odd part of n = 2^a b

@@ -22,14 +22,15 @@ namespace {
 constexpr int kRotThreads = 256;
 constexpr int kRotMaxN = 16384;
 constexpr int kBatch = 16;  // row elements per thread loaded together
+constexpr int kPadMaxN = 8192;
 
 __device__ __forceinline__ float load_f32(const float* p) { return *p; }
 __device__ __forceinline__ float load_f32(const __half* p) { return __half2float(*p); }
 
-template <int B, bool INV, class IT>
+template <int B, bool INV, bool PAD, class IT>
 __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t seed, float scale, const IT* x,
                                                              int64_t ldx, float* y, int64_t ldy, int64_t row0) {
-  extern __shared__ float buf[];  // n floats
+  extern __shared__ float buf[];  // n floats, or n + n/16 with PAD (padded slots, rot_slot)
   const int64_t row = row0 + blockIdx.x;
   const IT* xr = x + row * ldx;
   // loads in batches of kBatch per thread, all issued before the first is used, so a row's
@@ -44,21 +45,21 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t see
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int i = i0 + k * kRotThreads;
-      if (i < n) buf[i] = INV ? v[k] : v[k] * rot_sign(seed, i);
+      if (i < n) buf[rot_slot<PAD>(i)] = INV ? v[k] : v[k] * rot_sign(seed, i);
     }
   }
   __syncthreads();
   const int tid = threadIdx.x;
   if constexpr (!INV) {
     rot_odd_factor<B, false, kRotThreads>(buf, n, tid);
-    rot_hadamard<B, kRotThreads>(buf, n, tid);
+    rot_hadamard<B, kRotThreads, PAD>(buf, n, tid);
   } else {
-    rot_hadamard<B, kRotThreads>(buf, n, tid);
+    rot_hadamard<B, kRotThreads, PAD>(buf, n, tid);
     rot_odd_factor<B, true, kRotThreads>(buf, n, tid);
   }
   float* yr = y + row * ldy;
   for (int i = threadIdx.x; i < n; i += kRotThreads) {
-    const float v = buf[i] * scale;
+    const float v = buf[rot_slot<PAD>(i)] * scale;
     yr[i] = INV ? v * rot_sign(seed, i) : v;
   }
 }
@@ -70,8 +71,13 @@ hipError_t launch_rot(int n, uint64_t seed, const IT* x, int64_t ldx, float* y, 
   const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n / B)));  // 1 / sqrt(2^a)
   for (int64_t r0 = 0; r0 < m; r0 += kMaxGrid) {
     const int64_t g = (m - r0 < kMaxGrid) ? m - r0 : kMaxGrid;
-    hipLaunchKernelGGL((rotate_kernel<B, INV, IT>), dim3(static_cast<unsigned>(g)), dim3(kRotThreads),
-                       static_cast<unsigned>(n * sizeof(float)), s, n, seed, scale, x, ldx, y, ldy, r0);
+    // power-of-two rows up to kPadMaxN take the padded layout (at most 34 KB of LDS per row)
+    if (B == 1 && n <= kPadMaxN)
+      hipLaunchKernelGGL((rotate_kernel<B, INV, B == 1, IT>), dim3(static_cast<unsigned>(g)), dim3(kRotThreads),
+                         static_cast<unsigned>((n + (n >> 4)) * sizeof(float)), s, n, seed, scale, x, ldx, y, ldy, r0);
+    else
+      hipLaunchKernelGGL((rotate_kernel<B, INV, false, IT>), dim3(static_cast<unsigned>(g)), dim3(kRotThreads),
+                         static_cast<unsigned>(n * sizeof(float)), s, n, seed, scale, x, ldx, y, ldy, r0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
