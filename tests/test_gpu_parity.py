@@ -156,7 +156,8 @@ def test_decompose_replay_parity(n, k, dist):
 
 
 # ----------------------------------------------------------------------------- clustering and packing
-@pytest.mark.parametrize("n,k,lloyd", [(512, 20, 0), (768, 30, 0), (512, 20, 2), (4096, 30, 0), (96, 5, 3)])
+@pytest.mark.parametrize("n,k,lloyd", [(512, 20, 0), (768, 30, 0), (512, 20, 2), (4096, 30, 0), (96, 5, 3),
+                                         (3072, 20, 1), (11008, 8, 2)])
 def test_quantize_codes_and_reconstruct(n, k, lloyd):
     rng = np.random.default_rng(n + 100 * lloyd)
     m = 9
@@ -616,7 +617,8 @@ def test_rotated_quantization_pipeline():
 
 
 # ----------------------------------------------------------------------------- step schedules
-SCHED_CASES = [(n, s) for n in (512, 4096, 11008) for s in ("alternating", "reverse", "adaptive", "original")]
+SCHED_CASES = [(n, s) for n in (512, 4096, 11008) for s in ("alternating", "reverse", "adaptive", "original")] + \
+    [(768, "original"), (3072, "adaptive")]
 
 
 @pytest.mark.parametrize("n,schedule", SCHED_CASES)
