@@ -673,6 +673,13 @@ template <class C>
 constexpr bool compact_eps() {
   return has_split_pass<C>() || (C::W >= 4 && C::R0 == 16);  // split shape, or a 128-register budget
 }
+// vhat of the quantizer's block loop kept in private memory between its steps (16-byte loads and
+// stores of the whole array around the two vhat-steps of a block) rather than in registers, where
+// the 128-register budget would otherwise spill it value by value inside the transforms
+template <class C>
+constexpr bool vh_in_memory() {
+  return !has_split_pass<C>() && C::W >= 4 && C::R0 == 16 && C::E % 2 == 0;
+}
 template <class C, bool COMPACT>
 struct EpsRegs {
   float2 f[C::R0];
@@ -1509,6 +1516,27 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   };
 
   float2 z[C::E], vh[C::E];
+  constexpr bool VHM = vh_in_memory<C>();
+  float4 vhm[VHM ? C::E / 2 : 1];  // vhat between steps (VHM); a run-time index keeps it in memory
+  auto vh_store = [&]() {
+    if constexpr (VHM) {
+      const int b = opaque(0);
+#pragma unroll
+      for (int h = 0; h < C::E / 2; ++h)
+        vhm[b + h] = make_float4(vh[2 * h].x, vh[2 * h].y, vh[2 * h + 1].x, vh[2 * h + 1].y);
+    }
+  };
+  auto vh_load = [&]() {
+    if constexpr (VHM) {
+      const int b = opaque(0);
+#pragma unroll
+      for (int h = 0; h < C::E / 2; ++h) {
+        const float4 q = vhm[b + h];
+        vh[2 * h] = make_float2(q.x, q.y);
+        vh[2 * h + 1] = make_float2(q.z, q.w);
+      }
+    }
+  };
   if constexpr (ROT) {
 #pragma unroll
     for (int e = 0; e < C::E; ++e) z[e] = make_float2(0.f, 0.f);
@@ -1522,6 +1550,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   normalise_pair<C>(z, red, slot, scale, unscale, bad_a, bad_b);
 #pragma unroll
   for (int e = 0; e < C::E; ++e) vh[e] = make_float2(0.f, 0.f);
+  vh_store();
 
   const int steps = 4 * a.iters;
   int8_t* trace = nullptr;
@@ -1550,14 +1579,17 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
     csum_u = cadd(csum_u, c);
     // two steps on P Q_N, in the z = P rho domain, accumulating into vhat
     applyP(z);
+    vh_load();
     c = greedy_step<C, true>(z, vh, red, slot, tr ? tr + 2 * C::N : nullptr, side);
     step(t, 2, c);
     csum_v = cadd(csum_v, c);
     c = greedy_step<C, true>(z, vh, red, slot, tr ? tr + 3 * C::N : nullptr, side);
     step(t, 3, c);
     csum_v = cadd(csum_v, c);
+    vh_store();
   }
 
+  vh_load();
   // Epilogue.  vhat is consumed first (written out, or clustered into codes) so that it is
   // not live while u = w - P(z + vhat) is formed: the register peak stays that of the loop.
   const float qnan = __int_as_float(0x7fc00000);
