@@ -1559,10 +1559,15 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
     trace = a.tr_signs + (item * steps) * int64_t(C::N);
     trc = a.tr_c + item * steps;
   }
-  float2 cs[4];
+  // block-0 step sizes (equal in every lane): on the shapes whose block loop sits at its register
+  // limit they wait for the epilogue in LDS rather than in registers across the loop
+  constexpr bool CS_LDS = has_split_pass<C>() || is_small_inner_pass<C>(1) || vh_in_memory<C>();
+  __shared__ float2 cs_lds[4];
+  float2 cs_reg[4];
+  float2* cs = CS_LDS ? cs_lds : cs_reg;
   float2 csum_u = make_float2(0.f, 0.f), csum_v = make_float2(0.f, 0.f);
   auto step = [&](int t, int st, float2 c) {
-    if (t == 0) cs[st] = c;
+    if (t == 0 && (!CS_LDS || threadIdx.x == 0)) cs[st] = c;
     if constexpr (!QUANT) {
       if (trc != nullptr && threadIdx.x == 0) trc[4 * t + st] = (side ? c.y : c.x) * (side ? unscale.y : unscale.x);
     }
@@ -1590,6 +1595,7 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   }
 
   vh_load();
+  if constexpr (CS_LDS) __syncthreads();  // cs (written by thread 0 in the first block) visible to all
   // Epilogue.  vhat is consumed first (written out, or clustered into codes) so that it is
   // not live while u = w - P(z + vhat) is formed: the register peak stays that of the loop.
   const float qnan = __int_as_float(0x7fc00000);
