@@ -10,7 +10,7 @@ are not available here, so these matrices stand in for them with the same
 layer shapes and heavy-tailed value distributions.  Each row of an (M, N)
 matrix is one length-N vector (one output channel).
 
-Workloads (value recipe in the design doc):
+Workloads:
   ``gauss512``     256 x 512 fp32, N(0, 0.02^2), k = 20
   ``opt125m``      768x768 (x4), 3072x768, 768x3072 fp32, N(0, 0.02^2) with
                    0.1 % of columns scaled x20, k = 30
