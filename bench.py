@@ -237,7 +237,7 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: rows are independent, so a multi-GPU run would shard them "
-              "with no communication; only --gpus 1 is supported in this build.", file=sys.stderr)
+              "with no communication; only --gpus 1 is supported.", file=sys.stderr)
         return 2
 
     import torch
