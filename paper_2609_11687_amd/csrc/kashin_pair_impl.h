@@ -1329,12 +1329,8 @@ __device__ __forceinline__ void normalise_pair(float2 (&z)[C::E], float* red, in
   int ea = 0, eb = 0;
   if (!bad_a && v[0] > 0.f) (void)frexpf(v[0], &ea);
   if (!bad_b && v[1] > 0.f) (void)frexpf(v[1], &eb);
-  // equal in every lane: scalars (SGPRs), not per-lane registers kept across the block loop
-  auto uni = [](float x) { return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x))); };
-  scale = make_float2(uni(ldexpf(1.f, -ea)), uni(ldexpf(1.f, -eb)));
-  unscale = make_float2(uni(ldexpf(1.f, ea)), uni(ldexpf(1.f, eb)));
-  bad_a = __builtin_amdgcn_readfirstlane(bad_a ? 1 : 0) != 0;
-  bad_b = __builtin_amdgcn_readfirstlane(bad_b ? 1 : 0) != 0;
+  scale = make_float2(ldexpf(1.f, -ea), ldexpf(1.f, -eb));
+  unscale = make_float2(ldexpf(1.f, ea), ldexpf(1.f, eb));
 #pragma unroll
   for (int e = 0; e < C::E; ++e) {
     z[e].x = bad_a ? 0.f : z[e].x * scale.x;
