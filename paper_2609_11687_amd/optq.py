@@ -4,7 +4,8 @@ The columns of W (d_out x d_in) are the vectors quantised here; the matrix is he
 w_t = W^T (d_in x d_out), so that each column is a row of length d_out for the library kernels.
 Chunks of `chunk` columns are quantised at once (kashin_quantize: Alg. 2 + 2-bit clustering),
 dequantised (kashin_reconstruct), and their error Delta = W_c - Q_c is carried into the columns
-not yet quantised through the upper Cholesky factor U of (H + damp mean(diag H) I)^-1:
+not yet quantised through the upper Cholesky factor U of (H + damp mean(diag H) I)^-1
+(U_cc^-1 is the diagonal block of V = U^-1, see compensation_factor):
 
     W_r <- W_r - Delta U_cc^-1 U_cr        (held transposed: w_t[r] -= (U_cc^-1 U_cr)^T Delta^T)
 
@@ -18,14 +19,20 @@ from . import kashin as K
 
 
 def compensation_factor(h, damp: float = 0.01):
-    """U, the upper Cholesky factor of (H + damp mean(diag H) I)^-1 (float64, on H's device)."""
+    """(U, V): U the upper Cholesky factor of Hd^-1, Hd = H + damp mean(diag H) I, and V = U^-1
+    (float64, on H's device).  With J the exchange matrix, the lower Cholesky factor L of J Hd J
+    gives Hd = V V^T for the upper triangular V = J L J, so Hd^-1 = (V^-1)^T V^-1 and U = V^-1 (its
+    diagonal is positive): one factorisation and one triangular solve, without forming Hd^-1.
+    The diagonal blocks of V are the inverses of those of U."""
     import torch
 
     hd = h.to(torch.float64)
     d = hd.shape[0]
-    hd = hd + damp * hd.diagonal().mean() * torch.eye(d, dtype=torch.float64, device=hd.device)
-    hinv = torch.cholesky_inverse(torch.linalg.cholesky(hd))
-    return torch.linalg.cholesky(hinv, upper=True)
+    eye = torch.eye(d, dtype=torch.float64, device=hd.device)
+    hd = hd + damp * hd.diagonal().mean() * eye
+    v = torch.linalg.cholesky(hd.flip(0, 1)).flip(0, 1)
+    u = torch.linalg.solve_triangular(v, eye, upper=True)
+    return u, v
 
 
 def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iters: int = 0, record=None,
@@ -47,7 +54,7 @@ def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iter
         with torch.cuda.stream(stream):
             return optq_quantize(plan, w_t, h, chunk, damp, lloyd_iters, record, None)
     stream = torch.cuda.current_stream()
-    u = compensation_factor(h, damp)
+    u, v = compensation_factor(h, damp)
     nb = (d_out + 3) // 4
     cu = torch.empty((d_in, nb), dtype=torch.uint8, device=w_t.device)
     cv = torch.empty_like(cu)
@@ -61,7 +68,7 @@ def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iter
         K.kashin_reconstruct(plan, cu[c0:c1], cv[c0:c1], ce[c0:c1], q_t[c0:c1], stream)
         if c1 < d_in:
             delta = wc - q_t[c0:c1]
-            m = torch.linalg.solve_triangular(u[c0:c1, c0:c1], u[c0:c1, c1:], upper=True)
+            m = torch.matmul(v[c0:c1, c0:c1], u[c0:c1, c1:])  # U_cc^-1 U_cr
             w_t[c1:] -= torch.matmul(m.t().contiguous().to(torch.float32), delta)
         if snap is not None:
             snap["w_rest_after"] = w_t[c1:].clone()
