@@ -216,8 +216,8 @@ def per_n_figures(launches, launch_ms):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h", "schedule",
                                      "optq"), default="quantize")
