@@ -9,8 +9,9 @@
   matrices (--per-matrix: one kashin_quantize launch per matrix), inputs already resident in HBM.
 --op apply_p: one step = y = P x (kashin_apply_p) over --act-rows fp32 activation rows for each
   input width N of the workload (the inference-side product of App. C).
---op reconstruct: one step = w_hat = u_q + P v_q (kashin_reconstruct) from the codes and centres
-  of every matrix of the workload (quantized once, untimed).
+--op reconstruct: one step = w_hat = u_q + P v_q from the codes and centres of every matrix of
+  the workload (quantized once, untimed), one kashin_reconstruct_grouped launch per vector length
+  and 16 matrices (--per-matrix: one kashin_reconstruct launch per matrix).
 --op rotate: one step = the incoherence pre-rotation R w (kashin_rotate) of every matrix of the
   workload, fp16 rows in, fp32 rows out.
 --op quantize_h: one step = the "+H" pipeline, R w formed in the load, then quantised
@@ -226,8 +227,9 @@ def main() -> int:
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--per-matrix", action="store_true",
-                    help="--op quantize / quantize_h: one kashin_quantize(_rotated) launch per matrix instead "
-                         "of one kashin_quantize_grouped launch per vector length (up to 16 matrices each)")
+                    help="--op quantize / quantize_h / reconstruct: one kashin_quantize(_rotated) or "
+                         "kashin_reconstruct launch per matrix instead of one grouped launch per vector "
+                         "length (up to 16 matrices each)")
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -318,6 +320,8 @@ def main() -> int:
                     del wd
                     wh = torch.empty((spec.rows, spec.n), dtype=torch.float32, device=dev)
                     keep.append((plan, cu, cv, ce, wh))
+                    if not args.per_matrix:
+                        continue  # grouped by vector length below
                     launches.append(Launch(
                         spec.n, spec.rows, spec.rows * 2 * transform_flops(spec.n),
                         spec.rows * (2 * nb + 32 + 4 * spec.n),
@@ -337,6 +341,21 @@ def main() -> int:
                         lambda s, c=chunk: K.kashin_quantize_grouped(
                             c, args.lloyd, s, rot_seed=ROT_SEED if args.op == "quantize_h" else None),
                         wgs=sum((it[1].shape[0] + 1) // 2 for it in chunk)))
+        if args.op == "reconstruct" and not args.per_matrix:
+            # one grouped reconstruction per vector length and 16 matrices; each matrix takes a
+            # share of the persistent grid in proportion to its row pairs
+            for n in sorted({spec.n for spec in wl.matrices}):
+                items = [it for it in keep if it[0].n == n]
+                for c0 in range(0, len(items), 16):
+                    chunk = items[c0:c0 + 16]
+                    rows = sum(it[4].shape[0] for it in chunk)
+                    nb = (n + 3) // 4
+                    pairs = [(it[4].shape[0] + 1) // 2 for it in chunk]
+                    grid = min(sum(pairs), 2048)
+                    launches.append(Launch(
+                        n, rows, rows * 2 * transform_flops(n), rows * (2 * nb + 32 + 4 * n),
+                        lambda s, c=chunk: K.kashin_reconstruct_grouped(c, s), kind="pmap",
+                        wgs=sum(max(1, min(p, grid * p // sum(pairs))) for p in pairs)))
     elif args.op == "optq":
         from paper_2609_11687_amd import optq
 
@@ -455,7 +474,8 @@ def main() -> int:
     else:
         achieved = dom_bytes / dom_s / 1e9
         kname = f"rotate_kernel[b={dom_n // (dom_n & -dom_n)}]" if main_kind == "rotate" else "pair_pmap_kernel"
-        grid = (lambda l: l.rows) if main_kind == "rotate" else (lambda l: min((l.rows + 1) // 2, PMAP_GRID))
+        grid = (lambda l: l.rows) if main_kind == "rotate" else (
+            lambda l: l.wgs or min((l.rows + 1) // 2, PMAP_GRID))
         keyn = (lambda l: 0) if main_kind == "rotate" else (lambda l: l.n)  # the rotation kernel takes n at run time
         roofline = {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -475,7 +495,8 @@ def main() -> int:
         else:
             metric, unit = METRIC_RECON, "rows/s"
             workload = (f"reconstruct: {args.workload} {layer} from their 2+2-bit codes (k={wl.iters}), "
-                        f"fp32 output")
+                        f"fp32 output, " + ("one launch per matrix" if args.per_matrix else
+                                            "one grouped launch per vector length (kashin_reconstruct_grouped)"))
     result = {
         "metric": metric,
         "value": total_vectors / (ms_per_step / 1e3),

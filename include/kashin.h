@@ -99,6 +99,26 @@ int kashin_cluster2bit(kashin_plan_t plan, const float* u, const float* vhat, co
 int kashin_reconstruct(kashin_plan_t plan, const uint8_t* codes_u, const uint8_t* codes_v,
                        const float* centers, int64_t m, float* w_hat, int64_t ldw, void* stream);
 
+/* One matrix of kashin_reconstruct_grouped: the arguments kashin_reconstruct takes for it. */
+typedef struct {
+  kashin_plan_t plan;       /* every item's plan has the same n and lives on the same device */
+  const uint8_t* codes_u;   /* m x ceil(n/4) (device) */
+  const uint8_t* codes_v;   /* m x ceil(n/4) (device) */
+  const float* centers;     /* m x 2 x 4 (device) */
+  int64_t m;                /* >= 0; an item with m == 0 is skipped */
+  float* w_hat;             /* m rows of n fp32, leading dimension ldw >= n (device) */
+  int64_t ldw;
+} kashin_reconstruct_item;
+
+/* kashin_reconstruct over several matrices of one vector length, in one launch per 16 matrices
+ * (the load-time reconstitution of App. C for every matrix of a layer, each with its own plan).
+ * The launch's workgroups walk the row pairs of all matrices in order, loading a matrix's
+ * operator constants once per workgroup and matrix, so small matrices do not each pay a launch
+ * with its partial last wave.  Every matrix's w_hat equals kashin_reconstruct's bit for bit.
+ * items: host array of `count` entries (count >= 0), read before the call returns; nothing is
+ * allocated (the matrix table travels in the kernel arguments).  Output ranges must not overlap. */
+int kashin_reconstruct_grouped(const kashin_reconstruct_item* items, int32_t count, void* stream);
+
 /* The fused hot path: kashin_decompose followed by kashin_cluster2bit without writing the
  * factors: each row is read from HBM once and only codes and centres are written.
  * Same layouts as kashin_decompose (input) and kashin_cluster2bit (outputs). */

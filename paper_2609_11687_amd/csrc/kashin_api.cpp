@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -309,7 +310,7 @@ int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, in
     const kashin_quantize_item& it = items[i];
     if (it.m == 0) continue;
     a.group[g] = kashin::GroupItem{it.plan->d_tw, it.plan->d_mid, it.w, it.ldw, it.m, it.codes_u, it.codes_v,
-                                   it.centers, pairs};
+                                   it.centers, nullptr, 0, pairs, 0};
     pairs += (it.m + 1) / 2;
     if (++g == kashin::kMaxGroup || i == count - 1) {
       a.ngroup = g;
@@ -506,6 +507,54 @@ int kashin_reconstruct(kashin_plan_t plan, const uint8_t* codes_u, const uint8_t
   a.y = w_hat;
   a.ldy = ldw;
   return launch(plan, a, (m + 1) / 2, stream);
+}
+
+int kashin_reconstruct_grouped(const kashin_reconstruct_item* items, int32_t count, void* stream) {
+  if (count < 0) return fail(KASHIN_E_INVALID, "count must be >= 0 (got %d)", count);
+  if (count == 0) return ok();
+  if (items == nullptr) return fail(KASHIN_E_INVALID, "items is null");
+  const kashin_plan_s* p0 = nullptr;
+  for (int32_t i = 0; i < count; ++i) {
+    const kashin_reconstruct_item& it = items[i];
+    if (!live(it.plan)) return fail(KASHIN_E_INVALID, "item %d: plan is null or destroyed", i);
+    if (p0 == nullptr) {
+      p0 = it.plan;
+    } else if (it.plan->n != p0->n || it.plan->device != p0->device) {
+      return fail(KASHIN_E_INVALID, "item %d: plan (n %d, device %d) differs from item 0's (n %d, device %d)", i,
+                  it.plan->n, it.plan->device, p0->n, p0->device);
+    }
+    if (it.m < 0) return fail(KASHIN_E_INVALID, "item %d: m must be >= 0 (got %lld)", i, (long long)it.m);
+    if (it.ldw < p0->n) return fail(KASHIN_E_INVALID, "item %d: ldw (%lld) < n (%d)", i, (long long)it.ldw, p0->n);
+    if (it.m > 0 && (!it.codes_u || !it.codes_v || !it.centers || !it.w_hat))
+      return fail(KASHIN_E_INVALID, "item %d: codes, centers and w_hat must be non-null", i);
+  }
+  // launches of up to kMaxGroup non-empty matrices; each matrix gets a share of the persistent
+  // grid in proportion to its row pairs (at least one workgroup, at most one per pair)
+  std::vector<int32_t> idx;
+  for (int32_t i = 0; i < count; ++i)
+    if (items[i].m > 0) idx.push_back(i);
+  for (size_t c0 = 0; c0 < idx.size(); c0 += kashin::kMaxGroup) {
+    const size_t c1 = std::min(idx.size(), c0 + kashin::kMaxGroup);
+    int64_t pairs = 0;
+    for (size_t k = c0; k < c1; ++k) pairs += (items[idx[k]].m + 1) / 2;
+    const int64_t grid = std::min<int64_t>(pairs, kashin::kPmapGrid);
+    kashin::KArgs a = base_args(p0, kashin::MODE_RECON);
+    int64_t wg = 0, pair0 = 0;
+    for (size_t k = c0; k < c1; ++k) {
+      const kashin_reconstruct_item& it = items[idx[k]];
+      const int64_t np = (it.m + 1) / 2;
+      const int64_t nwg = std::max<int64_t>(1, std::min<int64_t>(np, grid * np / pairs));
+      a.group[k - c0] = kashin::GroupItem{it.plan->d_tw, it.plan->d_mid, it.codes_u, 0, it.m, nullptr,
+                                          const_cast<uint8_t*>(it.codes_v), const_cast<float*>(it.centers), it.w_hat,
+                                          it.ldw, pair0, wg};
+      wg += nwg;
+      pair0 += np;
+    }
+    a.ngroup = static_cast<int32_t>(c1 - c0);
+    const hipError_t e = kashin::launch_pair(p0->n, a, wg, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  }
+  return ok();
 }
 
 int kashin_cluster2bit(kashin_plan_t plan, const float* u, const float* vhat, const float* cstep, int64_t m,

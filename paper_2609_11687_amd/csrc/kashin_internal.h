@@ -23,8 +23,9 @@ enum Schedule : int32_t {
   SCHED_ORIGINAL = 3,     // Alg. 1: that choice, projection step ||.||_1 / nnz, stop at ||rho|| < tol
 };
 
-// One matrix of a grouped quantisation launch: its plan's tables, rows, outputs, and the index
-// of its first row pair among the launch's workgroups.
+// One matrix of a grouped launch: its plan's tables, rows, codes, centres, output rows, and the
+// index of its first row pair among the launch's items.  Quantisation reads w and writes the
+// codes and centres; reconstruction reads the codes (w = codes_u) and centres and writes y.
 struct GroupItem {
   const float2* tw;
   const float4* mid4;
@@ -34,9 +35,13 @@ struct GroupItem {
   uint8_t* codes_u;
   uint8_t* codes_v;
   float* centers;
+  float* y;
+  int64_t ldy;
   int64_t pair0;
+  int64_t wg0;  // reconstruction: the matrix's first workgroup (it takes wg0 .. next matrix's wg0 - 1)
 };
 constexpr int kMaxGroup = 16;  // matrices per grouped launch (the table travels in the kernel arguments)
+constexpr int64_t kPmapGrid = 2048;  // persistent y = P x / reconstruction grid: resident workgroups, a few times over
 
 // Everything a launch needs, passed to the kernel by value.
 struct KArgs {
@@ -77,8 +82,10 @@ struct KArgs {
   int32_t rot;
   float rot_scale;  // 1 / sqrt(2^a), n = 2^a b
   uint64_t rot_seed;
-  // MODE_QUANTIZE over several matrices of one vector length (ngroup > 0): workgroup p takes
-  // row pair p - group[g].pair0 of the last matrix g with group[g].pair0 <= p
+  // MODE_QUANTIZE over several matrices of one vector length (ngroup > 0): item p is row pair
+  // p - group[g].pair0 of the last matrix g with group[g].pair0 <= p.  MODE_RECON: workgroup b
+  // serves the last matrix g with group[g].wg0 <= b, walking its row pairs with the stride of
+  // that matrix's workgroup count
   int32_t ngroup;
   GroupItem group[kMaxGroup];
 };

@@ -1719,9 +1719,9 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
 // buffer, in row order, so codes are read one byte per four elements and w_hat is written in
 // contiguous 16-byte vectors; y = P x loads and stores in the register layout directly
 // (measured faster for it than staging).
-template <class C, bool ROT>
+template <class C, bool ROT, bool GROUPED>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) void pair_pmap_kernel(
-    KArgs a, int64_t item0, int64_t nitems) {
+    KArgs ka, int64_t item0, int64_t nitems) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
   __shared__ float red[2 * C::NW * 32];
   constexpr int N = C::N;
@@ -1730,13 +1730,34 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   int slot = 0;
   constexpr bool RES = resident_ok<C>();
   ResRegs<C> rr;
+  KArgs a = ka;
+  int64_t first = blockIdx.x, stride = gridDim.x;
+  if constexpr (GROUPED) {  // grouped reconstruction: this workgroup's matrix (uniform)
+    int gi = 0;
+#pragma unroll
+    for (int g = 1; g < kMaxGroup; ++g)
+      if (g < ka.ngroup && static_cast<int64_t>(blockIdx.x) >= ka.group[g].wg0) gi = g;
+    const GroupItem& gr = ka.group[gi];
+    a.tw = gr.tw;
+    a.mid4 = gr.mid4;
+    a.m = gr.m;
+    a.in_codes_v = gr.codes_v;
+    a.in_centers = gr.centers;
+    a.w = gr.w;  // codes_u
+    a.y = gr.y;
+    a.ldy = gr.ldy;
+    first = blockIdx.x - gr.wg0;
+    stride = (gi + 1 < ka.ngroup ? ka.group[gi + 1].wg0 : static_cast<int64_t>(gridDim.x)) - gr.wg0;
+    item0 = 0;
+    nitems = (gr.m + 1) / 2;
+  }
   if constexpr (RES) resident_load<C>(rr, lds, a.tw, a.mid4);
   const float qnan = __int_as_float(0x7fc00000);
   float* lf = reinterpret_cast<float*>(lds);  // staging: row a at [0, N), row b at [N, 2N)
   float4* lf4 = reinterpret_cast<float4*>(lds);
   const bool recon = a.mode == MODE_RECON;
   const bool vout = (reinterpret_cast<uintptr_t>(a.y) % 16 == 0) && (a.ldy % 4 == 0);
-  for (int64_t it = blockIdx.x; it < nitems; it += gridDim.x) {
+  for (int64_t it = first; it < nitems; it += stride) {
     const int64_t ra = 2 * (item0 + it);
     const int64_t rb = (ra + 1 < a.m) ? ra + 1 : -1;
     const int tid = opaque(bfly<C>(threadIdx.x));
@@ -2065,10 +2086,11 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
     } else if (a.mode == MODE_SCHEDULE) {
       hipLaunchKernelGGL(pair_schedule_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
     } else {
-      constexpr int64_t kPmapGrid = 2048;  // resident workgroups of the whole chip, a few times over
-      const int64_t pg = g < kPmapGrid ? g : kPmapGrid;
-      if (a.rot) hipLaunchKernelGGL((pair_pmap_kernel<C, true>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
-      else hipLaunchKernelGGL((pair_pmap_kernel<C, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      // grouped reconstruction: `grid` is the launch's workgroup count (the matrices' shares)
+      const int64_t pg = a.ngroup > 0 ? g : (g < kPmapGrid ? g : kPmapGrid);
+      if (a.rot) hipLaunchKernelGGL((pair_pmap_kernel<C, true, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      else if (a.ngroup > 0) hipLaunchKernelGGL((pair_pmap_kernel<C, false, true>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      else hipLaunchKernelGGL((pair_pmap_kernel<C, false, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

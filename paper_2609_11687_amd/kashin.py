@@ -24,7 +24,7 @@ KASHIN_F16 = 1
 EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
-    "kashin_quantize", "kashin_quantize_grouped", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
+    "kashin_quantize", "kashin_quantize_grouped", "kashin_reconstruct_grouped", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
     "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_status_string",
     "kashin_last_error",
 )
@@ -60,6 +60,7 @@ def lib() -> ctypes.CDLL:
         "kashin_reconstruct": [vp, vp, vp, vp, i64, vp, i64, vp],
         "kashin_quantize": [vp, vp, i32, i64, i64, i32, vp, vp, vp, vp],
         "kashin_quantize_grouped": [vp, i32, i32, i32, vp, vp],
+        "kashin_reconstruct_grouped": [vp, i32, vp],
         "kashin_apply_p": [vp, vp, vp, i64, vp],
         "kashin_rotate": [i32, u64, i32, vp, i32, i64, i64, vp, i64, vp],
         "kashin_quantize_rotated": [vp, u64, vp, i32, i64, i64, i32, vp, vp, vp, vp],
@@ -219,6 +220,22 @@ def kashin_quantize_grouped(items, lloyd_iters, stream=None, rot_seed=None):
     seed = None if rot_seed is None else ctypes.byref(ctypes.c_uint64(rot_seed))
     _check(lib().kashin_quantize_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), dtype, lloyd_iters, seed,
                                          _stream(stream)))
+
+
+class ReconstructItem(ctypes.Structure):
+    """kashin_reconstruct_item of include/kashin.h."""
+    _fields_ = [("plan", ctypes.c_void_p), ("codes_u", ctypes.c_void_p), ("codes_v", ctypes.c_void_p),
+                ("centers", ctypes.c_void_p), ("m", ctypes.c_int64), ("w_hat", ctypes.c_void_p),
+                ("ldw", ctypes.c_int64)]
+
+
+def kashin_reconstruct_grouped(items, stream=None):
+    """items: sequence of (plan, codes_u, codes_v, centers, w_hat), one per matrix."""
+    arr = (ReconstructItem * max(1, len(items)))()
+    for i, (plan, cu, cv, ce, wh) in enumerate(items):
+        m, ldw = _rows(wh)
+        arr[i] = ReconstructItem(plan.handle, cu.data_ptr(), cv.data_ptr(), ce.data_ptr(), m, wh.data_ptr(), ldw)
+    _check(lib().kashin_reconstruct_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), _stream(stream)))
 
 
 def kashin_apply_p(plan, x, y, stream=None):

@@ -163,3 +163,23 @@ def test_grouped_quantize_validation_before_device():
     assert "item 0" in L.kashin_last_error().decode()
     # the Python binding builds the same table from tensors
     assert ctypes.sizeof(K.QuantizeItem) == 56
+
+
+def test_grouped_reconstruct_validation_before_device():
+    """kashin_reconstruct_grouped checks its item table on the host: an empty table is a no-op, and
+    a null table, a negative count or an item with a dead plan is rejected before any launch."""
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1234)
+    buf = 0x1000
+    items = (K.ReconstructItem * 2)()
+    items[0] = K.ReconstructItem(fake, buf, buf, buf, 4, buf, 512)
+    items[1] = K.ReconstructItem(None, buf, buf, buf, 4, buf, 512)
+    table = ctypes.cast(items, ctypes.c_void_p)
+    assert L.kashin_reconstruct_grouped(table, 0, None) == K.KASHIN_OK
+    assert L.kashin_reconstruct_grouped(None, 0, None) == K.KASHIN_OK
+    assert L.kashin_reconstruct_grouped(None, 1, None) == K.KASHIN_E_INVALID
+    assert L.kashin_reconstruct_grouped(table, -1, None) == K.KASHIN_E_INVALID
+    assert L.kashin_reconstruct_grouped(table, 1, None) == K.KASHIN_E_INVALID
+    assert "item 0" in L.kashin_last_error().decode()
+    # the Python binding builds the same table from tensors
+    assert ctypes.sizeof(K.ReconstructItem) == 56

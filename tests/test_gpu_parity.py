@@ -304,6 +304,41 @@ def test_grouped_quantize_equals_per_matrix(n, k, dtype, lloyd, rows, rot):
         assert mu + mv <= max(1, int(2e-4 * tot))
 
 
+RECON_GROUPED = [(n, rows) for n, _, _, _, rows, rot in GROUPED if rot is None] + [
+    (256, [3000, 5, 2000]),  # more row pairs than the persistent grid: several pairs per workgroup
+    (4096, [700, 1, 1300]),
+]
+
+
+@pytest.mark.parametrize("n,rows", RECON_GROUPED)
+def test_grouped_reconstruct_equals_per_matrix(n, rows):
+    """kashin_reconstruct_grouped: every matrix (its own plan, codes and centres; one output
+    strided) gives kashin_reconstruct's w_hat on it alone, bit for bit, including matrices with
+    fewer row pairs than workgroups and ones whose workgroups take several pairs each."""
+    _say(f"grouped reconstruct N={n} rows={rows}")
+    rng = np.random.default_rng(n + 11)
+    items, ref_out = [], []
+    for i, m in enumerate(rows):
+        plan = K.kashin_plan(n, 2000 + 7 * i, 30)
+        w = pu.to_dev(_rows(rng, m, n, "t4" if i % 2 else "gauss"), torch.float32)
+        cu, cv, ce = K.quantize_alloc(plan, w, 0)
+        if i == 1 and m > 0:  # strided output rows: ld = n + 8
+            big = torch.full((m, n + 8), float("nan"), dtype=torch.float32, device="cuda")
+            wh = big[:, :n]
+        else:
+            wh = torch.full((m, n), float("nan"), dtype=torch.float32, device="cuda")
+        r1 = torch.empty((m, n), dtype=torch.float32, device="cuda")
+        K.kashin_reconstruct(plan, cu, cv, ce, r1)
+        items.append((plan, cu, cv, ce, wh))
+        ref_out.append(r1)
+    K.kashin_reconstruct_grouped(items)
+    torch.cuda.synchronize()
+    for i, ((plan, cu, cv, ce, wh), r1) in enumerate(zip(items, ref_out)):
+        assert torch.equal(wh.contiguous().view(torch.int32), r1.view(torch.int32)), f"matrix {i}: w_hat"
+    if len(rows) > 1 and rows[1] > 0:  # the padding of the strided output is left alone
+        assert torch.isnan(items[1][4].as_strided((rows[1], 8), (n + 8, 1), n)).all()
+
+
 # ----------------------------------------------------------------------------- properties and edges
 def test_deterministic_and_pow2_homogeneous():
     n, k, m = 512, 20, 6
