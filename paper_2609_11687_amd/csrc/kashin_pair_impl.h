@@ -1385,31 +1385,32 @@ __device__ __forceinline__ void cluster_factor(const float2 (&x)[C::E], float2 c
   closed_form(c1.x, c2.x, q[0]);
   closed_form(c1.y, c2.y, q[1]);
   if constexpr (LLOYD) {
+    // one row at a time, the four counts packed as bytes of one word (a thread holds fewer than
+    // 256 entries of a row): 5 accumulators live instead of 16, so the pass fits the registers
+    // the block loop leaves (sums and counts accumulate in the same order either way)
+    static_assert(C::E < 256, "per-thread counts packed in bytes");
     for (int it = 0; it < lloyd; ++it) {
-      float mids[2][3];
-      midpoints(q[0], mids[0]);
-      midpoints(q[1], mids[1]);
-      float acc[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) acc[k] = 0.f;
-      for_each_elem<C>([&](int e, int) {
-        const float xs[2] = {x[e].x, x[e].y};
-#pragma unroll
-        for (int sd = 0; sd < 2; ++sd) {
-          const int cd = code_of(xs[sd], mids[sd]);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            acc[sd * 8 + c] += (cd == c) ? xs[sd] : 0.f;
-            acc[sd * 8 + 4 + c] += (cd == c) ? 1.f : 0.f;
-          }
-        }
-      });
-      block_sum<C::T, 16>(acc, red, slot);
 #pragma unroll
       for (int sd = 0; sd < 2; ++sd) {
+        float mids[3];
+        midpoints(q[sd], mids);
+        float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+        uint32_t cnt = 0;
+        for_each_elem<C>([&](int e, int) {
+          const float xv = sd ? x[e].y : x[e].x;
+          const int cd = code_of(xv, mids);
+          s0 += (cd == 0) ? xv : 0.f;
+          s1 += (cd == 1) ? xv : 0.f;
+          s2 += (cd == 2) ? xv : 0.f;
+          s3 += (cd == 3) ? xv : 0.f;
+          cnt += 1u << (8 * cd);
+        });
+        float acc[8] = {s0, s1, s2, s3, static_cast<float>(cnt & 255u), static_cast<float>((cnt >> 8) & 255u),
+                        static_cast<float>((cnt >> 16) & 255u), static_cast<float>(cnt >> 24)};
+        block_sum<C::T, 8>(acc, red, slot);
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-          if (acc[sd * 8 + 4 + c] > 0.f) q[sd][c] = acc[sd * 8 + c] / acc[sd * 8 + 4 + c];
+          if (acc[4 + c] > 0.f) q[sd][c] = acc[c] / acc[4 + c];
         sort4(q[sd]);
       }
     }
