@@ -112,9 +112,10 @@ typedef struct {
 
 /* kashin_reconstruct over several matrices of one vector length, in one launch per 16 matrices
  * (the load-time reconstitution of App. C for every matrix of a layer, each with its own plan).
- * The launch's workgroups walk the row pairs of all matrices in order, loading a matrix's
- * operator constants once per workgroup and matrix, so small matrices do not each pay a launch
- * with its partial last wave.  Every matrix's w_hat equals kashin_reconstruct's bit for bit.
+ * The persistent grid is split between the matrices in proportion to their row pairs (at least
+ * one workgroup each, at most one per pair); a workgroup loads its matrix's operator constants
+ * once and walks that matrix's pairs, so small matrices do not each pay a launch with its partial
+ * last wave.  Every matrix's w_hat equals kashin_reconstruct's bit for bit.
  * items: host array of `count` entries (count >= 0), read before the call returns; nothing is
  * allocated (the matrix table travels in the kernel arguments).  Output ranges must not overlap. */
 int kashin_reconstruct_grouped(const kashin_reconstruct_item* items, int32_t count, void* stream);
