@@ -382,6 +382,9 @@ def main() -> int:
         keep.append(jobs)
         nchunks = sum((j[1].shape[0] + args.chunk - 1) // args.chunk for j in jobs)
 
+        # the longest chain of chunks (the widest d_in) is queued first, so the others overlap it
+        jobs.sort(key=lambda j: -j[1].shape[0])
+
         def run_optq(s):
             # every matrix on its own stream, joined back into the timing stream
             for plan, w0_t, w_t, hess, st in jobs:
