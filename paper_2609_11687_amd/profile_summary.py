@@ -27,10 +27,12 @@ COPY_BYTES = 256 << 20  # the calibration copy reads and writes 256 MiB
 
 
 def _short(name: str) -> tuple[str, int]:
-    m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|rotate_kernel|cluster_kernel|__amd_rocclr_copyBuffer\w*|"
-                  r"elementwise_kernel)", name)
+    m = re.search(r"(pair_greedy_kernel|pair_pmap_kernel|pair_schedule_kernel|rotate_kernel|cluster_kernel|"
+                  r"__amd_rocclr_copyBuffer\w*|elementwise_kernel|potf2\w*|\w*substitution\w*|Cijk_\w*)", name)
     c = re.search(r"Cfg<(\d+)", name)
     base = m.group(1) if m else name[:40]
+    if base.startswith("Cijk_"):  # library GEMM: operand layout, type and macro tile
+        base = base[:42]
     rot = re.search(r"rotate_kernel<(\d+), (true|false)", name)  # rotate_kernel<odd factor, inverse, input type>
     if rot:
         base += f"[b={rot.group(1)}" + (",inverse]" if rot.group(2) == "true" else "]")
@@ -75,6 +77,7 @@ def main() -> int:
     ap.add_argument("--copy-fetch")
     ap.add_argument("--copy-write")
     ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--top", type=int, default=0, help="list only the kernels with the largest total time")
     ap.add_argument("--bench-json", help="JSON line printed by the profiled bench run: its source_digest is "
                                          "recorded (default: the digest of the sources as they are now)")
     args = ap.parse_args()
@@ -90,11 +93,17 @@ def main() -> int:
     out.append("kernel trace (--kernel-trace --stats): average duration per dispatch")
     out.append(f"  {'kernel':28s} {'N':>6s} {'WGs':>6s} {'threads':>7s} {'calls':>5s} {'avg_us':>10s} "
                f"{'total_ms':>9s} {'scratch_B':>9s}")
-    for key in sorted(agg, key=lambda k: (-sum(agg[k]), k)):
+    keys = sorted(agg, key=lambda k: (-sum(agg[k]), k))
+    if args.top:
+        rest = keys[args.top:]
+        keys = keys[:args.top]
+    for key in keys:
         k, n, wg, wx = key
         v = agg[key]
         out.append(f"  {k:28s} {n:6d} {wg:6d} {wx:7d} {len(v):5d} {sum(v) / len(v) / 1e3:10.2f} "
                    f"{sum(v) / 1e6:9.3f} {meta[key]:9d}")
+    if args.top and rest:
+        out.append(f"  ({len(rest)} more kernel shapes, {sum(sum(agg[k]) for k in rest) / 1e6:.3f} ms in total)")
     traffic = None
     if args.fetch and args.write and args.copy_fetch and args.copy_write:
         fetch = counter_per_dispatch(args.fetch, "FETCH_SIZE")
