@@ -90,6 +90,8 @@ __all__ = [
     "SCHEDULES",
     "decompose_schedule",
     "synthetic_hessian",
+    "damped_hessian",
+    "compensation_factor",
     "optq_kashin",
     "optq_reference",
 ]
@@ -239,43 +241,31 @@ def decompose(w, eps, k, *, replay_signs=None, tau=None, trace=False):
             s = np.where(band, gs, s)
         return s
 
-    step = 0
-    for t in range(k):
-        # two greedy steps from Q_N: Delta u = sign(rho) * ||rho||_1 / N
-        for j in (0, 1):
-            x = rho
-            l1 = np.abs(x).sum(axis=1)
-            c = l1 / n
-            s = take_signs(x, c, step)
-            d = s * c[:, None]
-            if trace:
-                rec["r2_before"][:, step] = (rho * rho).sum(axis=1)
+    # Alg. 2 visits the two halves of the dictionary in a fixed cycle of four atomic steps: the
+    # cube Q_N twice, then its image P Q_N twice.  An atom of the cube half is a sign vector
+    # itself; an atom of the other half is P applied to one, so its correlation with the residual
+    # is read off P rho, and removing it subtracts P Delta from rho.
+    cycle = ("cube", "cube", "rotated", "rotated")
+    for step in range(nsteps):
+        half = cycle[step % 4]
+        x = rho if half == "cube" else apply_p(rho, eps)
+        l1 = np.abs(x).sum(axis=1)
+        c = l1 / n  # step size ||x||_1 / N; sign(0) = 0 below
+        s = take_signs(x, c, step)
+        d = s * c[:, None]
+        if trace:
+            rec["r2_before"][:, step] = (rho * rho).sum(axis=1)
+        if half == "cube":
             u += d
             rho = rho - d
-            if trace:
-                _record(rec, step, c, l1, x, s, rho)
-            if t == 0:
-                cstep[:, j] = c
-            csum[:, 0] += c
-            step += 1
-        # two greedy steps from P Q_N: Delta vhat = sign(P rho) * ||P rho||_1 / N,
-        # rho <- rho - P Delta vhat
-        for j in (2, 3):
-            x = apply_p(rho, eps)
-            l1 = np.abs(x).sum(axis=1)
-            c = l1 / n
-            s = take_signs(x, c, step)
-            d = s * c[:, None]
-            if trace:
-                rec["r2_before"][:, step] = (rho * rho).sum(axis=1)
+        else:
             vhat += d
             rho = rho - apply_p(d, eps)
-            if trace:
-                _record(rec, step, c, l1, x, s, rho)
-            if t == 0:
-                cstep[:, j] = c
-            csum[:, 1] += c
-            step += 1
+        if trace:
+            _record(rec, step, c, l1, x, s, rho)
+        if step < 4:
+            cstep[:, step] = c  # Sec. 3.1: the first block's four magnitudes fix the centres
+        csum[:, 0 if half == "cube" else 1] += c
     out = {"u": u, "vhat": vhat, "r": rho, "cstep": cstep, "csum": csum}
     if trace:
         out["trace"] = rec
@@ -607,9 +597,18 @@ def synthetic_hessian(d: int, nsamples: int, seed: int, outlier_cols: int = 0, o
     return x.T @ x / nsamples
 
 
-def _damped(h, damp):
+def damped_hessian(h, damp=0.01):
+    """H + lambda I with lambda = damp * mean(diag H): the 1 % damping of the compensation (a
+    remark in Sec. 5 sets damp = 0.01)."""
     h = np.asarray(h, dtype=np.float64)
     return h + damp * np.mean(np.diag(h)) * np.eye(h.shape[0])
+
+
+def compensation_factor(h, damp=0.01):
+    """Upper-triangular U with U^T U = (H + lambda I)^-1: the Cholesky factor of the damped
+    inverse Hessian whose rows carry a quantised chunk's error forward (eq. optq_update)."""
+    hinv = np.linalg.inv(damped_hessian(h, damp))
+    return np.linalg.cholesky(hinv).T
 
 
 def _quantise_columns(cols, eps, k, lloyd_iters):
@@ -619,20 +618,26 @@ def _quantise_columns(cols, eps, k, lloyd_iters):
     return reconstruct(unpack2bit(cu, n), unpack2bit(cv, n), centers, eps), (cu, cv, centers)
 
 
-def optq_kashin(w, h, eps, k, chunk, damp=0.01, lloyd_iters=0):
+def optq_kashin(w, h, eps, k, chunk, damp=0.01, lloyd_iters=0, quantiser=None):
     """W (d_out, d_in), H (d_in, d_in): quantise the columns of W (vectors of length d_out) in
     chunks of `chunk` columns; after each chunk c, with Delta = W_c - Q_c and U the upper Cholesky
     factor of (H + damp mean(diag H) I)^-1, the remaining columns become W_r - Delta U_cc^-1 U_cr.
-    Returns (Q, W_final, codes) with codes = per chunk (codes_u, codes_v, centers)."""
+    Returns (Q, W_final, codes) with codes = per chunk (codes_u, codes_v, centers).
+
+    ``quantiser(cols, c0)`` (optional) replaces the column quantiser: it maps the chunk starting
+    at column c0 (one column vector per row of ``cols``) to (dequantised rows, codes); a test uses
+    it to replay another implementation's near-tie decisions chunk by chunk."""
     w = np.array(w, dtype=np.float64, copy=True)
     d_in = w.shape[1]
-    hinv = np.linalg.inv(_damped(h, damp))
-    u = np.linalg.cholesky(hinv).T  # hinv = u^T u, u upper triangular
+    u = compensation_factor(h, damp)  # hinv = u^T u, u upper triangular
     q = np.zeros_like(w)
     codes = []
     for c0 in range(0, d_in, chunk):
         c1 = min(c0 + chunk, d_in)
-        qc, cd = _quantise_columns(w[:, c0:c1].T, eps, k, lloyd_iters)
+        if quantiser is None:
+            qc, cd = _quantise_columns(w[:, c0:c1].T, eps, k, lloyd_iters)
+        else:
+            qc, cd = quantiser(w[:, c0:c1].T, c0)
         q[:, c0:c1] = qc.T
         codes.append(cd)
         delta = w[:, c0:c1] - q[:, c0:c1]
@@ -648,7 +653,7 @@ def optq_reference(w, h, chunk, quantiser, damp=0.01):
     dequantised values.  With chunk = 1 the update is eq. optq_update with [H^-1]_ii."""
     w = np.array(w, dtype=np.float64, copy=True)
     d_in = w.shape[1]
-    g = np.linalg.inv(_damped(h, damp))
+    g = np.linalg.inv(damped_hessian(h, damp))
     q = np.zeros_like(w)
     for c0 in range(0, d_in, chunk):
         c1 = min(c0 + chunk, d_in)

@@ -311,6 +311,25 @@ def test_lloyd_between_closed_form_and_optimum(rng):
             prev = cur
 
 
+def test_lloyd_keeps_an_emptied_centre():
+    """Sec. 3.1's refinement, hand-solved: a cluster that receives no value keeps its previous
+    centre (it is neither dropped, zeroed nor moved), the others move to their means, and the
+    result stays sorted.  Midpoints of [-3, -1, 1, 3] are -2, 0, 2."""
+    q0 = np.array([[-3.0, -1.0, 1.0, 3.0]])
+    # clusters 1 and 2 empty: both inner centres kept
+    np.testing.assert_array_equal(ref.lloyd(np.array([[-3.0, -3.0, 3.0, 3.0]]), q0, 1), q0)
+    # cluster 1 empty (kept at -1); clusters 0, 2, 3 take the means -2.5, 0.5 and 4
+    x = np.array([[-2.5, -2.5, 0.5, 4.0, 4.0]])
+    np.testing.assert_array_equal(ref.lloyd(x, q0, 1), [[-2.5, -1.0, 0.5, 4.0]])
+    # a second pass from there: midpoints -1.75, -0.25, 2.25 give the same clusters
+    np.testing.assert_array_equal(ref.lloyd(x, q0, 2), [[-2.5, -1.0, 0.5, 4.0]])
+    # closed form with equal steps (inner centres both 0): clusters 1 and 3 empty
+    qd = ref.closed_form_centers(np.array([0.5]), np.array([0.5]))
+    out = ref.lloyd(np.array([[0.3, 0.3, -0.7]]), qd, 1)
+    np.testing.assert_array_equal(out, [[-0.7, 0.0, 0.3, 1.0]])
+    assert np.all(np.diff(out, axis=1) >= 0)
+
+
 def test_assign_ties_go_low():
     q = np.array([[-3.0, -1.0, 1.0, 3.0]])
     x = np.array([[-2.0, 0.0, 2.0, -2.0000001, 2.0000001, 5.0, -5.0]])
@@ -542,6 +561,44 @@ def test_optq_cholesky_form_equals_hessian_downdate(chunk):
     q2, wf2 = ref.optq_reference(w, h, chunk, _quantiser(eps, k))
     np.testing.assert_allclose(q, q2, rtol=0, atol=1e-12)
     np.testing.assert_allclose(wf, wf2, rtol=0, atol=1e-12)
+
+
+def test_damping_and_factor_by_hand():
+    """The 1 % damping adds lambda = 0.01 mean(diag H) to the diagonal: for H = diag(1, 3),
+    lambda = 0.02; the factor U (upper, U^T U = (H + lambda I)^-1) is then diag(1/sqrt(1.02),
+    1/sqrt(3.02)).  A full 2x2 case: H = [[2, 1], [1, 2]], lambda = 0.02, so H + lambda I =
+    [[2.02, 1], [1, 2.02]] with inverse [[2.02, -1], [-1, 2.02]] / (2.02^2 - 1); its Cholesky factor
+    (lower, L L^T) has L_11 = sqrt(2.02 / det), L_21 = -1 / (det L_11), and U = L^T."""
+    h = np.diag([1.0, 3.0])
+    np.testing.assert_allclose(ref.damped_hessian(h), np.diag([1.02, 3.02]), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(ref.compensation_factor(h), np.diag([1 / np.sqrt(1.02), 1 / np.sqrt(3.02)]),
+                               rtol=1e-15)
+    h2 = np.array([[2.0, 1.0], [1.0, 2.0]])
+    det = 2.02 ** 2 - 1.0
+    l11 = np.sqrt(2.02 / det)
+    l21 = -1.0 / (det * l11)
+    l22 = np.sqrt(2.02 / det - l21 ** 2)
+    np.testing.assert_allclose(ref.compensation_factor(h2), [[l11, l21], [0.0, l22]], rtol=1e-14, atol=1e-15)
+    # no damping: the factor of H^-1 itself
+    np.testing.assert_allclose(ref.compensation_factor(h, damp=0.0), np.diag([1.0, 1 / np.sqrt(3.0)]), rtol=1e-15)
+
+
+def test_optq_chunk1_two_columns_by_hand(rng):
+    """Two columns, chunk 1: the second column receives the first one's error scaled by
+    -[(H + lambda I)^-1]_01 / [(H + lambda I)^-1]_00 (eq. optq_update for one column), worked out
+    here from the 2x2 inverse rather than through the factor: -(-h01/det) / (h11/det) = h01 / h11
+    with h = H + lambda I."""
+    dout, k = 32, 5
+    w = rng.standard_normal((dout, 2)) * 0.02
+    eps = ref.sign_mask(dout, 4)
+    h = np.array([[3.0, 1.2], [1.2, 2.0]])
+    hd = h + 0.01 * 2.5 * np.eye(2)
+    q, wf, _ = ref.optq_kashin(w, h, eps, k, 1)
+    q0 = _quantiser(eps, k)(w[:, :1].T).T
+    np.testing.assert_allclose(q[:, :1], q0, atol=1e-15)
+    expect = w[:, 1] - (w[:, 0] - q0[:, 0]) * (-hd[0, 1] / hd[1, 1])
+    np.testing.assert_allclose(wf[:, 1], expect, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(q[:, 1:], _quantiser(eps, k)(expect[None, :]).T, atol=1e-15)
 
 
 def test_optq_without_correlation_or_with_one_chunk_is_plain_quantisation(rng):
