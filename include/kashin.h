@@ -49,7 +49,15 @@ enum {
 
 enum { KASHIN_F32 = 0, KASHIN_F16 = 1 };
 
-/* 1 if vectors of length n have a compiled kernel, else 0.  Host only, no device needed. */
+/* 1 if vectors of length n have a compiled kernel, else 0.  Host only, no device needed.
+ * The supported lengths are exactly
+ *     64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 5120, 6144, 8192, 10000, 11008,
+ *     13824, 14336, 16384
+ * (the row widths of the OPT, Llama-2, Pythia and Mistral layers of Sec. 5, the N = 10^4 of the
+ * convergence comparison of Sec. 4.1, and small lengths for tests).  Each has a transform shape
+ * compiled for it (a mixed-radix FFT over radices 2, 3, 4, 5, 7, 8, 9, 12, 16 and 43);
+ * other lengths, even ones whose factors are all available, return 0.  A row pair of length N
+ * occupies 8N bytes of LDS, so no length above about 19800 can be added on gfx950 (160 KB). */
 int kashin_supported_n(int32_t n);
 
 /* The sign mask eps in {-1,+1}^n for `seed` (Sec. 4.1 T_E; Sec. 5 / App. C: one mask per
@@ -204,7 +212,9 @@ int kashin_rotate(int32_t n, uint64_t seed, int32_t inverse, const void* x, int3
 /* The "+H" pipeline with the rotation fused: kashin_quantize of R w (R as kashin_rotate with
  * seed rot_seed; n = the plan's length), the rows rotated on the way in, so w is read once and the
  * rotated rows are never written.  Codes and centres are those of R w; results equal
- * kashin_rotate followed by kashin_quantize of its fp32 output bit for bit. */
+ * kashin_rotate followed by kashin_quantize of its fp32 output bit for bit.  Plans whose length
+ * kashin_rotate does not take (odd part other than 1, 3 or 43) return KASHIN_E_UNSUPPORTED_N; so
+ * do kashin_reconstruct_rotated and kashin_quantize_grouped with a rotation seed. */
 int kashin_quantize_rotated(kashin_plan_t plan, uint64_t rot_seed, const void* w, int32_t dtype, int64_t m,
                             int64_t ldw, int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers,
                             void* stream);

@@ -79,7 +79,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 4)))
     # biggest translation units first
-    order = sorted(srcs, key=lambda p: ("11008" not in p, "172" not in p, "16384" not in p, p))
+    order = sorted(srcs, key=lambda p: ("11008" not in p, "13824" not in p, "14336" not in p, "16384" not in p, p))
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), order))
     tmp = LIB + ".tmp"

@@ -303,7 +303,11 @@ int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, in
   kashin::KArgs a = base_args(p0, kashin::MODE_QUANTIZE);
   a.dtype = dtype;
   a.lloyd = lloyd_iters;
-  if (rot_seed != nullptr) set_rotation(&a, p0->n, *rot_seed);
+  if (rot_seed != nullptr) {
+    if (!kashin::rotate_supported_n(p0->n))
+      return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", p0->n);
+    set_rotation(&a, p0->n, *rot_seed);
+  }
   int32_t g = 0;
   int64_t pairs = 0;
   for (int32_t i = 0; i < count; ++i) {
@@ -434,6 +438,8 @@ int kashin_quantize_rotated(kashin_plan_t plan, uint64_t rot_seed, const void* w
                             void* stream) {
   int st = check_common(plan, m);
   if (st) return st;
+  if (!kashin::rotate_supported_n(plan->n))
+    return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", plan->n);
   if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
@@ -456,6 +462,8 @@ int kashin_reconstruct_rotated(kashin_plan_t plan, uint64_t rot_seed, const uint
                                const float* centers, int64_t m, float* w_hat, int64_t ldw, void* stream) {
   int st = check_common(plan, m);
   if (st) return st;
+  if (!kashin::rotate_supported_n(plan->n))
+    return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", plan->n);
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (m == 0) return ok();
   if (!codes_u || !codes_v || !centers || !w_hat) return fail(KASHIN_E_INVALID, "codes, centers and w_hat must be non-null");

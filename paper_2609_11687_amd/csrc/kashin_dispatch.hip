@@ -16,8 +16,13 @@ namespace kashin {
   X(2048, 128, 2, 16, 8, 16)        \
   X(3072, 256, 3, 16, 12, 16)      \
   X(4096, 256, 3, 16, 16, 16)       \
+  X(5120, 320, 3, 16, 16, 4, 5)     \
+  X(6144, 384, 3, 16, 16, 8, 3)     \
   X(8192, 512, 2, 16, 16, 16, 2)    \
+  X(10000, 640, 3, 16, 5, 5, 5, 5)  \
   X(11008, 768, 3, 16, 43, 16)      \
+  X(13824, 448, 2, 16, 16, 2, 3, 9) \
+  X(14336, 448, 2, 16, 16, 8, 7)    \
   X(16384, 1024, 4, 16, 8, 8, 16)
 
 #define X(N, ...) hipError_t launch_n##N(const KArgs& a, int64_t grid, hipStream_t stream);

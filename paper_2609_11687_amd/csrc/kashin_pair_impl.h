@@ -1135,13 +1135,20 @@ __device__ __forceinline__ void apply_P_res(float2 (&z)[C::E], float2* lds, RR& 
 
 // ------------------------------------------------------------------ greedy step
 __device__ __forceinline__ int8_t sgn8(float x) { return x > 0.f ? 1 : (x < 0.f ? -1 : 0); }
-// sign(x) * c with sign(0) = 0
-__device__ __forceinline__ float sgn_times(float x, float c) { return x == 0.f ? 0.f : copysignf(c, x); }
+// sign(x) * c with sign(0) = 0, as the median of (-c, x 2^160, c): every nonzero float times 2^160
+// is at least 2^11 in magnitude (or infinite), above any step size c -- on the normalised rows
+// (max |w| < 1) c <= ||x||_2 <= ||w||_2 < sqrt(N) < 2^8, since no step raises the residual norm --
+// so the median is exactly +-c; x = +-0 gives +-0, and x -/+ 0 leaves x unchanged up to the sign
+// of a zero.  Two VALU operations instead of a compare, a copysign and a select.
+__device__ __forceinline__ float sgn_times(float x, float c) {
+  return __builtin_amdgcn_fmed3f(-c, __builtin_amdgcn_ldexpf(x, 160), c);
+}
 
+// s / N: exact for a power of two; otherwise s times the float nearest 1 / N (within one ulp of the
+// quotient, and the step size c only enters the greedy as c itself)
 template <int N>
 __device__ __forceinline__ float div_n(float s) {
-  if constexpr ((N & (N - 1)) == 0) return s * (1.0f / N);  // exact: same bits as s / N
-  else return s / static_cast<float>(N);
+  return s * static_cast<float>(1.0 / N);
 }
 
 // One atomic greedy step of Alg. 2 on both rows: c = ||x||_1 / N, delta = sign(x) c
@@ -1329,6 +1336,10 @@ __device__ __forceinline__ void normalise_pair(float2 (&z)[C::E], float* red, in
   int ea = 0, eb = 0;
   if (!bad_a && v[0] > 0.f) (void)frexpf(v[0], &ea);
   if (!bad_b && v[1] > 0.f) (void)frexpf(v[1], &eb);
+  // a row of subnormals only (max below 2^-126) would need a scale above 2^126: clamp, so that the
+  // scale stays finite and the scaled row stays finite and nonzero (it is then below 0.5)
+  ea = ea < -126 ? -126 : ea;
+  eb = eb < -126 ? -126 : eb;
   scale = make_float2(ldexpf(1.f, -ea), ldexpf(1.f, -eb));
   unscale = make_float2(ldexpf(1.f, ea), ldexpf(1.f, eb));
 #pragma unroll
@@ -2071,17 +2082,34 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
 }
 
 // ------------------------------------------------------------------ dispatch
+// Whether the incoherence rotation of length N can be fused into the pair kernels: the odd
+// factor C_b has compile-time constants for b = 1, 3 and 43 only (the lengths the rotation kernel
+// takes); the host layer rejects the rotated entry points for other lengths before any launch.
+constexpr bool rot_fusable(int n) {
+  const int b = n / (n & -n);
+  return n <= 16384 && (b == 1 || b == 3 || b == 43);
+}
+
 template <class C>
 hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
   constexpr int64_t kMaxGrid = int64_t(1) << 30;
+  if constexpr (!rot_fusable(C::N)) {
+    if (a.rot) return hipErrorInvalidValue;
+  }
   for (int64_t i0 = 0; i0 < grid; i0 += kMaxGrid) {
     const int64_t g = (grid - i0 < kMaxGrid) ? grid - i0 : kMaxGrid;
     const dim3 gd(static_cast<unsigned>(g)), bd(C::T);
     if (a.mode == MODE_QUANTIZE) {
-      if (a.lloyd > 0 && a.rot) hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, true>), gd, bd, 0, s, a, i0);
-      else if (a.lloyd > 0) hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, false>), gd, bd, 0, s, a, i0);
-      else if (a.rot) hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, true>), gd, bd, 0, s, a, i0);
-      else hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, false>), gd, bd, 0, s, a, i0);
+      if (a.rot) {
+        if constexpr (rot_fusable(C::N)) {
+          if (a.lloyd > 0) hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, true>), gd, bd, 0, s, a, i0);
+          else hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, true>), gd, bd, 0, s, a, i0);
+        }
+      } else if (a.lloyd > 0) {
+        hipLaunchKernelGGL((pair_greedy_kernel<C, true, true, false>), gd, bd, 0, s, a, i0);
+      } else {
+        hipLaunchKernelGGL((pair_greedy_kernel<C, false, true, false>), gd, bd, 0, s, a, i0);
+      }
     } else if (a.mode <= MODE_TRACE) {
       hipLaunchKernelGGL((pair_greedy_kernel<C, false, false, false>), gd, bd, 0, s, a, i0);
     } else if (a.mode == MODE_SCHEDULE) {
@@ -2089,8 +2117,10 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
     } else {
       // grouped reconstruction: `grid` is the launch's workgroup count (the matrices' shares)
       const int64_t pg = a.ngroup > 0 ? g : (g < kPmapGrid ? g : kPmapGrid);
-      if (a.rot) hipLaunchKernelGGL((pair_pmap_kernel<C, true, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
-      else if (a.ngroup > 0) hipLaunchKernelGGL((pair_pmap_kernel<C, false, true>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      if (a.rot) {
+        if constexpr (rot_fusable(C::N))
+          hipLaunchKernelGGL((pair_pmap_kernel<C, true, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
+      } else if (a.ngroup > 0) hipLaunchKernelGGL((pair_pmap_kernel<C, false, true>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
       else hipLaunchKernelGGL((pair_pmap_kernel<C, false, false>), dim3(static_cast<unsigned>(pg)), bd, 0, s, a, i0, g);
     }
     const hipError_t e = hipGetLastError();

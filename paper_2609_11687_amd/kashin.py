@@ -117,14 +117,75 @@ def _rows(w):
     return w.shape[0], w.stride(0)
 
 
+def _on_plan_device(plan, t, name):
+    if t.device.type != "cuda" or (plan is not None and t.device.index != plan.device):
+        where = "cuda" if plan is None else f"cuda:{plan.device}"
+        raise ValueError(f"{name} must live on {where} (got {t.device})")
+
+
+def _need(plan, t, shape, dtype, name, nullable=False):
+    """Check an output or side input the library reads or writes with a fixed layout: exact shape,
+    dtype, contiguous, on the plan's device.  The C side trusts these (a wrong buffer would be a
+    device out-of-bounds access), so they are checked before every call."""
+    import torch
+
+    if t is None:
+        if nullable:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if t.numel():
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        _on_plan_device(plan, t, name)
+
+
+def _need_rows(plan, w, n, name, dtypes=None):
+    """A row-major input or output of m rows of n entries (unit-stride rows, any ld >= n)."""
+    import torch
+
+    m, ld = _rows(w)
+    if w.shape[1] != n:
+        raise ValueError(f"{name} rows must have {n} entries (got {w.shape[1]})")
+    if dtypes is not None and w.dtype not in dtypes:
+        raise TypeError(f"{name} must be one of {dtypes} (got {w.dtype})")
+    if m:
+        _on_plan_device(plan, w, name)
+    return m, ld
+
+
+def _f32():
+    import torch
+    return torch.float32
+
+
+def _codes_shapes(plan, m):
+    import torch
+    nb = (plan.n + 3) // 4
+    return (m, nb), torch.uint8, (m, 2, 4), torch.float32
+
+
+def _need_codes(plan, m, codes_u, codes_v, centers):
+    cs, cdt, ces, cedt = _codes_shapes(plan, m)
+    _need(plan, codes_u, cs, cdt, "codes_u")
+    _need(plan, codes_v, cs, cdt, "codes_v")
+    _need(plan, centers, ces, cedt, "centers")
+
+
 class Plan:
     """Owns a kashin_plan_t; destroyed explicitly (``destroy``) or on garbage collection."""
 
-    def __init__(self, handle: ctypes.c_void_p, n: int, seed: int, iters: int):
+    def __init__(self, handle: ctypes.c_void_p, n: int, seed: int, iters: int, device: int = 0):
         self.handle = handle
         self.n = n
         self.seed = seed
         self.iters = iters
+        self.device = device  # the HIP device the plan's tables live on (current at creation)
 
     def destroy(self) -> None:
         if self.handle:
@@ -153,9 +214,10 @@ def kashin_signs(n: int, seed: int):
 
 # ----------------------------------------------------------------------------- plan
 def kashin_plan(n: int, seed: int, iters: int) -> Plan:
+    import torch
     h = ctypes.c_void_p()
     _check(lib().kashin_plan(ctypes.byref(h), n, seed, iters))
-    return Plan(h, n, seed, iters)
+    return Plan(h, n, seed, iters, torch.cuda.current_device())
 
 
 def kashin_plan_destroy(plan: Plan) -> None:
@@ -177,25 +239,40 @@ def kashin_plan_info(plan: Plan):
 
 # ----------------------------------------------------------------------------- device calls
 def kashin_decompose(plan, w, u, vhat, r=None, cstep=None, bounds=None, stream=None):
-    m, ldw = _rows(w)
+    import torch
+    m, ldw = _need_rows(plan, w, plan.n, "w", (torch.float32, torch.float16))
+    for name, t, nl in (("u", u, False), ("vhat", vhat, False), ("r", r, True)):
+        _need(plan, t, (m, plan.n), torch.float32, name, nullable=nl)
+    _need(plan, cstep, (m, 4), torch.float32, "cstep", nullable=True)
+    _need(plan, bounds, (m, 4), torch.float32, "bounds", nullable=True)
     _check(lib().kashin_decompose(plan.handle, _ptr(w), _dtype_code(w), m, ldw, _ptr(u), _ptr(vhat), _ptr(r),
                                   _ptr(cstep), _ptr(bounds), _stream(stream)))
 
 
 def kashin_cluster2bit(plan, u, vhat, cstep, lloyd_iters, codes_u, codes_v, centers, stream=None):
+    import torch
     m = u.shape[0]
+    _need(plan, u, (m, plan.n), torch.float32, "u")
+    _need(plan, vhat, (m, plan.n), torch.float32, "vhat")
+    _need(plan, cstep, (m, 4), torch.float32, "cstep")
+    cs, cdt, ces, cedt = _codes_shapes(plan, m)
+    _need(plan, codes_u, cs, cdt, "codes_u")
+    _need(plan, codes_v, cs, cdt, "codes_v")
+    _need(plan, centers, ces, cedt, "centers")
     _check(lib().kashin_cluster2bit(plan.handle, _ptr(u), _ptr(vhat), _ptr(cstep), m, lloyd_iters, _ptr(codes_u),
                                     _ptr(codes_v), _ptr(centers), _stream(stream)))
 
 
 def kashin_reconstruct(plan, codes_u, codes_v, centers, w_hat, stream=None):
-    m, ldw = _rows(w_hat)
+    m, ldw = _need_rows(plan, w_hat, plan.n, "w_hat", (_f32(),))
+    _need_codes(plan, m, codes_u, codes_v, centers)
     _check(lib().kashin_reconstruct(plan.handle, _ptr(codes_u), _ptr(codes_v), _ptr(centers), m, _ptr(w_hat), ldw,
                                     _stream(stream)))
 
 
 def kashin_quantize(plan, w, lloyd_iters, codes_u, codes_v, centers, stream=None):
-    m, ldw = _rows(w)
+    m, ldw = _need_rows(plan, w, plan.n, "w")
+    _need_codes(plan, m, codes_u, codes_v, centers)
     _check(lib().kashin_quantize(plan.handle, _ptr(w), _dtype_code(w), m, ldw, lloyd_iters, _ptr(codes_u),
                                  _ptr(codes_v), _ptr(centers), _stream(stream)))
 
@@ -212,7 +289,8 @@ def kashin_quantize_grouped(items, lloyd_iters, stream=None, rot_seed=None):
     arr = (QuantizeItem * max(1, len(items)))()
     dtype = KASHIN_F32
     for i, (plan, w, cu, cv, ce) in enumerate(items):
-        m, ldw = _rows(w)
+        m, ldw = _need_rows(plan, w, plan.n, f"items[{i}].w")
+        _need_codes(plan, m, cu, cv, ce)
         dtype = _dtype_code(w)
         arr[i] = QuantizeItem(plan.handle, w.data_ptr(), m, ldw, cu.data_ptr(), cv.data_ptr(), ce.data_ptr())
     if any(_dtype_code(it[1]) != dtype for it in items):
@@ -233,46 +311,62 @@ def kashin_reconstruct_grouped(items, stream=None):
     """items: sequence of (plan, codes_u, codes_v, centers, w_hat), one per matrix."""
     arr = (ReconstructItem * max(1, len(items)))()
     for i, (plan, cu, cv, ce, wh) in enumerate(items):
-        m, ldw = _rows(wh)
+        m, ldw = _need_rows(plan, wh, plan.n, f"items[{i}].w_hat", (_f32(),))
+        _need_codes(plan, m, cu, cv, ce)
         arr[i] = ReconstructItem(plan.handle, cu.data_ptr(), cv.data_ptr(), ce.data_ptr(), m, wh.data_ptr(), ldw)
     _check(lib().kashin_reconstruct_grouped(ctypes.cast(arr, ctypes.c_void_p), len(items), _stream(stream)))
 
 
 def kashin_apply_p(plan, x, y, stream=None):
     m = x.shape[0]
+    _need(plan, x, (m, plan.n), _f32(), "x")
+    _need(plan, y, (m, plan.n), _f32(), "y")
     _check(lib().kashin_apply_p(plan.handle, _ptr(x), _ptr(y), m, _stream(stream)))
 
 
 def kashin_decompose_schedule(plan, schedule, w, u, vhat, r=None, tol=0.0, stream=None):
-    m, ldw = _rows(w)
+    m, ldw = _need_rows(plan, w, plan.n, "w")
+    for name, t, nl in (("u", u, False), ("vhat", vhat, False), ("r", r, True)):
+        _need(plan, t, (m, plan.n), _f32(), name, nullable=nl)
     _check(lib().kashin_decompose_schedule(plan.handle, SCHEDULES[schedule], tol, _ptr(w), _dtype_code(w), m, ldw,
                                            _ptr(u), _ptr(vhat), _ptr(r), _stream(stream)))
 
 
 def kashin_trace_schedule(plan, schedule, w, rows, sign_trace, c_trace, choice_trace, r2_trace, u, vhat, tol=0.0,
                           stream=None):
-    m, ldw = _rows(w)
+    import torch
+    m, ldw = _need_rows(plan, w, plan.n, "w")
+    nr, st = rows.numel(), 4 * plan.iters
+    _need(plan, rows, (nr,), torch.int64, "rows")
+    _need(plan, sign_trace, (nr, st, plan.n), torch.int8, "sign_trace")
+    _need(plan, c_trace, (nr, st), torch.float32, "c_trace")
+    _need(plan, choice_trace, (nr, st), torch.int8, "choice_trace")
+    _need(plan, r2_trace, (nr, st), torch.float32, "r2_trace")
+    _need(plan, u, (nr, plan.n), torch.float32, "u")
+    _need(plan, vhat, (nr, plan.n), torch.float32, "vhat")
     _check(lib().kashin_trace_schedule(plan.handle, SCHEDULES[schedule], tol, _ptr(w), _dtype_code(w), m, ldw,
                                        _ptr(rows), rows.numel(), _ptr(sign_trace), _ptr(c_trace), _ptr(choice_trace),
                                        _ptr(r2_trace), _ptr(u), _ptr(vhat), _stream(stream)))
 
 
 def kashin_quantize_rotated(plan, rot_seed, w, lloyd_iters, codes_u, codes_v, centers, stream=None):
-    m, ldw = _rows(w)
+    m, ldw = _need_rows(plan, w, plan.n, "w")
+    _need_codes(plan, m, codes_u, codes_v, centers)
     _check(lib().kashin_quantize_rotated(plan.handle, rot_seed, _ptr(w), _dtype_code(w), m, ldw, lloyd_iters,
                                          _ptr(codes_u), _ptr(codes_v), _ptr(centers), _stream(stream)))
 
 
 def kashin_reconstruct_rotated(plan, rot_seed, codes_u, codes_v, centers, w_hat, stream=None):
-    m, ldw = _rows(w_hat)
+    m, ldw = _need_rows(plan, w_hat, plan.n, "w_hat", (_f32(),))
+    _need_codes(plan, m, codes_u, codes_v, centers)
     _check(lib().kashin_reconstruct_rotated(plan.handle, rot_seed, _ptr(codes_u), _ptr(codes_v), _ptr(centers), m,
                                             _ptr(w_hat), ldw, _stream(stream)))
 
 
 def kashin_rotate(n, seed, x, y, inverse=False, stream=None):
     """y = R x (or R^T x) row-wise; x fp32 or fp16 rows, y fp32 rows (y may be x, fp32)."""
-    m, ldx = _rows(x)
-    my, ldy = _rows(y)
+    m, ldx = _need_rows(None, x, n, "x")
+    my, ldy = _need_rows(None, y, n, "y", (_f32(),))
     if my != m:
         raise ValueError("x and y must have the same number of rows")
     _check(lib().kashin_rotate(n, seed, 1 if inverse else 0, _ptr(x), _dtype_code(x), m, ldx, _ptr(y), ldy,
@@ -280,7 +374,14 @@ def kashin_rotate(n, seed, x, y, inverse=False, stream=None):
 
 
 def kashin_trace(plan, w, rows, sign_trace, c_trace, u, vhat, stream=None):
-    m, ldw = _rows(w)
+    import torch
+    m, ldw = _need_rows(plan, w, plan.n, "w")
+    nr, st = rows.numel(), 4 * plan.iters
+    _need(plan, rows, (nr,), torch.int64, "rows")
+    _need(plan, sign_trace, (nr, st, plan.n), torch.int8, "sign_trace")
+    _need(plan, c_trace, (nr, st), torch.float32, "c_trace")
+    _need(plan, u, (nr, plan.n), torch.float32, "u")
+    _need(plan, vhat, (nr, plan.n), torch.float32, "vhat")
     _check(lib().kashin_trace(plan.handle, _ptr(w), _dtype_code(w), m, ldw, _ptr(rows), rows.numel(),
                               _ptr(sign_trace), _ptr(c_trace), _ptr(u), _ptr(vhat), _stream(stream)))
 

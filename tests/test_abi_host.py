@@ -29,12 +29,32 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(K.EXPORTS)
 
 
-@pytest.mark.parametrize("n", [64, 96, 172, 512, 768, 1024, 3072, 4096, 11008, 16384])
+def _documented_lengths():
+    """The supported set as the header states it (the comment of kashin_supported_n)."""
+    text = open(HEADER).read()
+    block = text[text.index("The supported lengths are exactly"):text.index("int kashin_supported_n")]
+    block = block[:block.index("(")]
+    return sorted(int(v) for v in re.findall(r"\b\d+\b", block))
+
+
+def test_supported_lengths_are_exactly_the_documented_set():
+    """The length contract: kashin_supported_n is 1 exactly on the set the header lists (every
+    integer up to 40000 is asked), and that set holds the widths of the paper's models and its
+    N = 10^4 convergence set-up."""
+    doc = _documented_lengths()
+    got = [n for n in range(0, 40001) if K.kashin_supported_n(n)]
+    assert got == doc
+    for n in (768, 3072, 4096, 11008, 5120, 13824, 14336, 16384, 2048, 8192, 10000):
+        assert n in got
+
+
+@pytest.mark.parametrize("n", [64, 96, 172, 512, 768, 1024, 3072, 4096, 5120, 6144, 10000, 11008, 13824, 14336,
+                               16384])
 def test_supported_sizes(n):
     assert K.kashin_supported_n(n)
 
 
-@pytest.mark.parametrize("n", [0, 1, 2, 7, 100, 4095, 4097, 32768])
+@pytest.mark.parametrize("n", [-4, 0, 1, 2, 7, 100, 4095, 4097, 12288, 20000, 28672, 32768])
 def test_unsupported_sizes(n):
     assert not K.kashin_supported_n(n)
 
@@ -126,8 +146,9 @@ def test_schedule_validation_before_device():
 
 
 def test_rotated_entry_points_reject_dead_plan():
-    """The fused-rotation entry points validate the plan like their unrotated forms (the
-    rotation itself needs no argument beyond the seed: every plan length has odd part 1, 3 or 43)."""
+    """The fused-rotation entry points validate the plan like their unrotated forms (dead plans
+    first; the plan's length is checked against the rotation's after that, which needs a live
+    plan, hence a device: see the GPU tests)."""
     L = K.lib()
     fake = ctypes.c_void_p(0x1234)
     buf = ctypes.c_void_p(0x1000)
@@ -137,10 +158,19 @@ def test_rotated_entry_points_reject_dead_plan():
     assert "plan" in L.kashin_last_error().decode()
 
 
-@pytest.mark.parametrize("n", [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 8192, 11008, 16384])
-def test_every_plan_length_is_rotatable(n):
-    assert K.kashin_supported_n(n)
-    assert n // (n & -n) in (1, 3, 43)
+@pytest.mark.parametrize("n", [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 5120, 6144, 8192, 10000, 11008,
+                               13824, 14336, 16384])
+def test_rotation_lengths(n):
+    """The rotation takes the plan lengths whose odd part is 1, 3 or 43; the others (odd parts 5,
+    625, 27 and 7) are rejected on the host with KASHIN_E_UNSUPPORTED_N."""
+    L = K.lib()
+    x = ctypes.c_void_p(0x10000)
+    y = ctypes.c_void_p(0x10000000)
+    st = L.kashin_rotate(n, 0, 0, x, 0, 0, n, y, n, None)  # m = 0: validated, nothing launched
+    if n // (n & -n) in (1, 3, 43):
+        assert st == K.KASHIN_OK
+    else:
+        assert st == K.KASHIN_E_UNSUPPORTED_N
 
 
 def test_grouped_quantize_validation_before_device():
@@ -183,3 +213,38 @@ def test_grouped_reconstruct_validation_before_device():
     assert "item 0" in L.kashin_last_error().decode()
     # the Python binding builds the same table from tensors
     assert ctypes.sizeof(K.ReconstructItem) == 56
+
+
+def test_binding_checks_buffers_before_calling():
+    """The binding rejects output buffers of the wrong shape, dtype or layout, and tensors off the
+    plan's device, before calling into the library (the C side trusts the layouts it documents).
+    Zero-row tensors reach the shape checks without a device."""
+    import torch
+
+    plan = K.Plan(None, 512, 0, 4, 0)
+    w0 = torch.zeros((0, 512), dtype=torch.float32)
+    cu, cv, ce = torch.zeros((0, 128), dtype=torch.uint8), torch.zeros((0, 128), dtype=torch.uint8), \
+        torch.zeros((0, 2, 4), dtype=torch.float32)
+    with pytest.raises(ValueError, match="shape"):
+        K.kashin_quantize(plan, w0, 0, torch.zeros((0, 127), dtype=torch.uint8), cv, ce)
+    with pytest.raises(TypeError, match="uint8"):
+        K.kashin_quantize(plan, w0, 0, torch.zeros((0, 128), dtype=torch.int8), cv, ce)
+    with pytest.raises(ValueError, match="shape"):
+        K.kashin_quantize(plan, w0, 0, cu, cv, torch.zeros((0, 8), dtype=torch.float32))
+    with pytest.raises(ValueError, match="entries"):
+        K.kashin_quantize(plan, torch.zeros((0, 256), dtype=torch.float32), 0, cu, cv, ce)
+    with pytest.raises(ValueError, match="shape"):
+        K.kashin_decompose(plan, w0, w0, torch.zeros((0, 511), dtype=torch.float32))
+    with pytest.raises(ValueError, match="required"):
+        K.kashin_decompose(plan, w0, w0, None)
+    with pytest.raises(ValueError, match="shape"):
+        K.kashin_trace(plan, w0, torch.zeros(0, dtype=torch.int64), torch.zeros((0, 16, 512), dtype=torch.int8),
+                       torch.zeros((0, 15), dtype=torch.float32), torch.zeros((0, 512)), torch.zeros((0, 512)))
+    # a non-contiguous output and a host tensor with rows: rejected before any call
+    with pytest.raises(ValueError, match="contiguous"):
+        K.kashin_apply_p(plan, torch.zeros((512, 2), dtype=torch.float32).t(), torch.zeros((2, 512)))
+    with pytest.raises(ValueError, match="cuda"):
+        K.kashin_quantize(plan, torch.zeros((2, 512), dtype=torch.float32), 0, cu, cv, ce)
+    # all layouts right: the call reaches the library, which rejects the null plan
+    with pytest.raises(K.KashinError):
+        K.kashin_quantize(plan, w0, 0, cu, cv, ce, stream=0)
