@@ -9,9 +9,15 @@ not yet quantised through the upper Cholesky factor U of (H + damp mean(diag H) 
 
     W_r <- W_r - Delta U_cc^-1 U_cr        (held transposed: w_t[r] -= (U_cc^-1 U_cr)^T Delta^T)
 
-With chunk = 1 this is eq. optq_update column by column.  The factorisation of the d_in x d_in
-Hessian (float64) and the trailing update (an fp32 GEMM) use the ROCm libraries through torch;
-every decomposition, clustering and reconstruction runs in libkashin.
+With chunk = 1 this is eq. optq_update column by column.  With exact=True the columns of a chunk
+are quantised one at a time and each one's error reaches the chunk's later columns before they are
+quantised (err_i = Delta_i / U_ii, w_j -= err_i U_ij inside the chunk); the chunk's errors reach
+the remaining columns in one product at the chunk's end (W_r -= E U_cr): OPTQ's lazy block
+update, which equals eq. optq_update applied column by column for any chunk size.  The chunk
+form (exact=False) quantises a chunk's columns together, which is exact only at chunk = 1.
+The factorisation of the d_in x d_in Hessian (float64) and the trailing update (an fp32 GEMM)
+use the ROCm libraries through torch; every decomposition, clustering and reconstruction runs in
+libkashin.
 """
 from __future__ import annotations
 
@@ -36,7 +42,7 @@ def compensation_factor(h, damp: float = 0.01):
 
 
 def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iters: int = 0, record=None,
-                  stream=None):
+                  stream=None, exact: bool = False):
     """Quantise the rows of w_t (d_in x d_out fp32, CUDA; the columns of W) with error
     compensation; w_t is updated in place to the compensated weights.  Returns
     (codes_u, codes_v, centers, q_t) for all d_in rows (q_t = the dequantised rows).
@@ -52,7 +58,7 @@ def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iter
         raise ValueError("w_t must be contiguous fp32")
     if stream is not None:
         with torch.cuda.stream(stream):
-            return optq_quantize(plan, w_t, h, chunk, damp, lloyd_iters, record, None)
+            return optq_quantize(plan, w_t, h, chunk, damp, lloyd_iters, record, None, exact)
     stream = torch.cuda.current_stream()
     u, v = compensation_factor(h, damp)
     nb = (d_out + 3) // 4
@@ -60,9 +66,26 @@ def optq_quantize(plan, w_t, h, chunk: int = 128, damp: float = 0.01, lloyd_iter
     cv = torch.empty_like(cu)
     ce = torch.empty((d_in, 2, 4), dtype=torch.float32, device=w_t.device)
     q_t = torch.empty_like(w_t)
+    u32 = u.to(torch.float32) if exact else None
     for c0 in range(0, d_in, chunk):
         c1 = min(c0 + chunk, d_in)
         wc = w_t[c0:c1]
+        if exact:
+            # one column at a time; its error reaches the chunk's later columns at once
+            for i in range(c0, c1):
+                if record is not None:
+                    record.append({"c0": i, "c1": i + 1, "w_chunk": w_t[i:i + 1].clone()})
+                K.kashin_quantize(plan, w_t[i:i + 1], lloyd_iters, cu[i:i + 1], cv[i:i + 1], ce[i:i + 1], stream)
+                K.kashin_reconstruct(plan, cu[i:i + 1], cv[i:i + 1], ce[i:i + 1], q_t[i:i + 1], stream)
+                if i + 1 < c1:
+                    err = (w_t[i] - q_t[i]) / u32[i, i]
+                    w_t[i + 1:c1] -= torch.outer(u32[i, i + 1:c1], err)
+            if c1 < d_in:
+                err = (wc - q_t[c0:c1]) / u32[c0:c1, c0:c1].diagonal()[:, None]  # E, chunk x d_out
+                w_t[c1:] -= torch.matmul(u32[c0:c1, c1:].t().contiguous(), err)
+            if record is not None:
+                record[-1]["w_rest_after"] = w_t[c1:].clone()
+            continue
         snap = {"c0": c0, "c1": c1, "w_chunk": wc.clone()} if record is not None else None
         K.kashin_quantize(plan, wc, lloyd_iters, cu[c0:c1], cv[c0:c1], ce[c0:c1], stream)
         K.kashin_reconstruct(plan, cu[c0:c1], cv[c0:c1], ce[c0:c1], q_t[c0:c1], stream)

@@ -17,7 +17,7 @@ import parity_util as pu
 
 pytestmark = pytest.mark.gpu
 
-ALL_N = [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 8192, 11008, 16384]
+ALL_N = [64, 96, 172, 256, 512, 768, 1024, 2048, 3072, 4096, 5120, 6144, 8192, 10000, 11008, 13824, 14336, 16384]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -116,13 +116,16 @@ def test_reconstruct_layer_sampled_rows():
 # ----------------------------------------------------------------------------- Alg. 2 on small batches
 CASES = [(64, 3, "gauss"), (96, 20, "gauss"), (172, 20, "t4"), (256, 1, "gauss"), (512, 20, "gauss"),
          (768, 30, "outlier"), (1024, 8, "t4"), (2048, 20, "gauss"), (3072, 30, "outlier"), (4096, 30, "t4"),
-         (11008, 4, "outlier")]
+         (5120, 20, "gauss"), (6144, 12, "t4"), (8192, 30, "t4"), (10000, 20, "gauss"), (11008, 4, "outlier"),
+         (11008, 30, "t4"), (13824, 8, "outlier"), (14336, 8, "t4"), (16384, 30, "gauss")]
 
 
 @pytest.mark.parametrize("n,k,dist", CASES)
 def test_decompose_replay_parity(n, k, dist):
+    """kashin_decompose (u, vhat, r, block-0 step sizes, factor bounds) against the oracle replayed
+    on the GPU's near-tie signs, on every transform shape (odd row count: an unpaired last row)."""
     rng = np.random.default_rng(7 * n + k)
-    m = 7
+    m = 7 if n * k <= 100000 else 3
     w = _rows(rng, m, n, dist)
     seed = 17 + n
     eps = ref.sign_mask(n, seed)
@@ -137,7 +140,7 @@ def test_decompose_replay_parity(n, k, dist):
     w64 = w.astype(np.float64)
     res = pu.replay_parity(w64, eps, k, signs, u.astype(np.float64), vh.astype(np.float64))
     _say(f"decompose N={n} k={k} {dist}: du={res['du'].max():.2e} dv={res['dv'].max():.2e} "
-         f"rec={res['rec'].max():.2e} in-band flips={res['in_band_flips'].sum()} direct ok={res['direct_frac_ok']:.2f}")
+         f"rec={res['rec'].max():.2e} in-band flips={res['in_band_flips'].sum()} direct ok={res['direct_frac_ok']}")
     pu.assert_replay_ok(res, f"N={n}")
     rep = res["rep"]
     winf = res["winf"]
@@ -240,7 +243,12 @@ GROUPED = [  # (n, k, dtype, lloyd, rows per matrix, rotation seed): sizes on ev
     (4096, 30, torch.float16, 0, [6, 0, 3, 10], None),
     (11008, 30, torch.float16, 0, [3, 2, 0, 5], None),
     (16384, 8, torch.float32, 0, [2, 3], None),
+    (5120, 10, torch.float16, 0, [3, 4], None),
+    (10000, 6, torch.float32, 1, [3, 0, 2], None),
+    (13824, 4, torch.float16, 0, [2, 3], None),
+    (14336, 4, torch.float32, 2, [3, 2], None),
     (768, 30, torch.float32, 0, [5, 4], 99),
+    (6144, 10, torch.float16, 0, [3, 2], 99),
     (4096, 30, torch.float16, 0, [6, 3, 1], 99),
     (11008, 30, torch.float16, 0, [3, 4], 99),
 ]
@@ -453,6 +461,135 @@ def test_nonfinite_row_is_isolated():
         assert rec <= 1e-5 * np.abs(w[row]).max()
 
 
+def test_lloyd_keeps_emptied_centres_fused():
+    """Rows a s with s in {-1,1}^N and a = 2^-6 (every sum exact in fp32): one u-step takes the
+    whole row (u = w, c1 = a, every later step 0), so the closed-form centres are [-a, -a, a, a],
+    the codes are 0 and 2, and Lloyd passes leave clusters 1 and 3 (and three clusters of vhat = 0)
+    empty.  The fused quantizer's codes and centres equal the oracle's exactly, for 1 and 2 passes
+    (an emptied cluster keeps its centre: Sec. 3.1)."""
+    n, k = 512, 3
+    rng = np.random.default_rng(3)
+    s = np.where(rng.random((5, n)) < 0.5, -1.0, 1.0)
+    w = (2.0 ** -6 * s).astype(np.float32)
+    w[4] = 2.0 ** -6  # a constant row: a single occupied cluster
+    seed = 77
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, k)
+    wd = pu.to_dev(w)
+    d = ref.decompose(w.astype(np.float64), eps, k)
+    for lloyd in (1, 2):
+        cu, cv, ce = K.quantize_alloc(plan, wd, lloyd)
+        torch.cuda.synchronize()
+        ru, rv, rc = ref.cluster2bit(d["u"], d["vhat"], d["cstep"], lloyd)
+        np.testing.assert_array_equal(ce.cpu().numpy(), rc.astype(np.float32))
+        np.testing.assert_array_equal(pu.unpack(cu.cpu().numpy(), n), ru)
+        np.testing.assert_array_equal(pu.unpack(cv.cpu().numpy(), n), rv)
+        np.testing.assert_array_equal(rc[0, 0], [-2.0 ** -6, -2.0 ** -6, 2.0 ** -6, 2.0 ** -6])
+
+
+def test_lloyd_keeps_emptied_centres_standalone():
+    """kashin_cluster2bit on hand-built factors (values exact in fp32): u rows with values -2.5, 0.5
+    and 4 around the closed-form centres [-3, -1, 1, 3] (c1 = 2, c2 = 1) leave cluster 1 empty,
+    vhat rows with -3.5, -0.75 and 2.5 leave cluster 2 empty; one and two Lloyd passes give the
+    oracle's centres and codes exactly (the emptied centre is kept)."""
+    n, m = 64, 3
+    rng = np.random.default_rng(4)
+    u = np.concatenate([np.full(16, -2.5), np.full(16, 0.5), np.full(32, 4.0)])
+    v = np.concatenate([np.full(20, -3.5), np.full(20, -0.75), np.full(24, 2.5)])
+    uu = np.stack([rng.permutation(u) for _ in range(m)]).astype(np.float32)
+    vv = np.stack([rng.permutation(v) for _ in range(m)]).astype(np.float32)
+    cs = np.tile(np.array([2.0, 1.0, 2.0, 1.0], np.float32), (m, 1))
+    plan = K.kashin_plan(n, 1, 1)
+    for lloyd in (1, 2):
+        cu = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
+        cv = torch.empty_like(cu)
+        ce = torch.empty((m, 2, 4), dtype=torch.float32, device="cuda")
+        K.kashin_cluster2bit(plan, pu.to_dev(uu), pu.to_dev(vv), pu.to_dev(cs), lloyd, cu, cv, ce)
+        torch.cuda.synchronize()
+        ru, rv, rc = ref.cluster2bit(uu, vv, cs, lloyd)
+        np.testing.assert_array_equal(rc[0, 0], [-2.5, -1.0, 0.5, 4.0])
+        np.testing.assert_array_equal(rc[0, 1], [-3.5, -0.75, 1.0, 2.5])
+        np.testing.assert_array_equal(ce.cpu().numpy(), rc.astype(np.float32))
+        np.testing.assert_array_equal(pu.unpack(cu.cpu().numpy(), n), ru)
+        np.testing.assert_array_equal(pu.unpack(cv.cpu().numpy(), n), rv)
+
+
+def test_subnormal_row():
+    """A fp32 row whose entries are all subnormal (|w| < 2^-126): the row scale is clamped so it
+    stays finite; factors and centres are finite and equal those of the same row scaled by 2^126
+    (a normal row: the decomposition is homogeneous), divided back, to fp32 resolution of the
+    normal row.  Each row is decomposed alone (no partner)."""
+    n, k = 512, 10
+    rng = np.random.default_rng(8)
+    tiny = (rng.standard_normal(n) * 1e-40).astype(np.float32)
+    assert np.abs(tiny).max() < 2.0 ** -126 and np.count_nonzero(tiny) > n // 2
+    big = (tiny.astype(np.float64) * 2.0 ** 126).astype(np.float32)
+    np.testing.assert_array_equal(big.astype(np.float64) * 2.0 ** -126, tiny.astype(np.float64))
+    plan = K.kashin_plan(n, 3, k)
+    outs = []
+    for row in (tiny, big):
+        wd = pu.to_dev(row[None, :])
+        u, vh, _, cs, _ = K.decompose_alloc(plan, wd)
+        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy().astype(np.float64) for t in (u, vh, cs, ce)])
+    for t in outs[0]:
+        assert np.isfinite(t).all()
+    scale = np.abs(big).max()
+    for a, b in zip(outs[0], outs[1]):
+        err = np.abs(a * 2.0 ** 126 - b).max() / scale
+        assert err <= 1e-5, err
+    # and the normal row against the oracle
+    eps = ref.sign_mask(n, 3)
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, pu.to_dev(big[None, :]), [0], k)
+    pu.assert_replay_ok(pu.replay_parity(big[None, :].astype(np.float64), eps, k, signs, u_tr, v_tr), "normal")
+
+
+def test_row_pairing_permutation():
+    """A row's last bits depend on the row it shares a complex FFT with.  Quantising the rows in a
+    permuted order (every row gets another partner) changes nothing beyond that: both orders pass
+    the replay parity against the oracle row by row, and their codes differ only where the
+    parity rule allows (near a decision boundary, at most 1e-4 of the codes)."""
+    n, k, m = 1024, 20, 12
+    rng = np.random.default_rng(31)
+    w = _rows(rng, m, n, "t4")
+    perm = rng.permutation(m)
+    seed = 55
+    eps = ref.sign_mask(n, seed)
+    plan = K.kashin_plan(n, seed, k)
+    w64 = w.astype(np.float64)
+    codes = []
+    for order in (np.arange(m), perm):
+        wd = pu.to_dev(w[order])
+        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+        signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, list(range(m)), k)
+        res = pu.replay_parity(w64[order], eps, k, signs, u_tr, v_tr)
+        pu.assert_replay_ok(res, "pairing")
+        inv = np.argsort(order)
+        codes.append((pu.unpack(cu.cpu().numpy(), n)[inv], pu.unpack(cv.cpu().numpy(), n)[inv],
+                      ce.cpu().numpy()[inv]))
+    diff = int((codes[0][0] != codes[1][0]).sum() + (codes[0][1] != codes[1][1]).sum())
+    _say(f"pairing permutation: {diff} of {2 * m * n} codes differ")
+    assert diff <= max(1, int(1e-4 * 2 * m * n))
+    np.testing.assert_allclose(codes[0][2], codes[1][2], rtol=1e-5, atol=1e-7)
+
+
+def test_rotation_rejected_for_other_odd_parts():
+    """Plans whose length has an odd part other than 1, 3 or 43 take every entry point except the
+    rotated ones, which return KASHIN_E_UNSUPPORTED_N before launching anything."""
+    for n in (5120, 10000, 13824, 14336):
+        plan = K.kashin_plan(n, 1, 2)
+        wd = torch.zeros((2, n), dtype=torch.float32, device="cuda")
+        cu, cv, ce = K.quantize_alloc(plan, wd, 0)
+        for call in (lambda: K.kashin_quantize_rotated(plan, 5, wd, 0, cu, cv, ce),
+                     lambda: K.kashin_reconstruct_rotated(plan, 5, cu, cv, ce, wd),
+                     lambda: K.kashin_quantize_grouped([(plan, wd, cu, cv, ce)], 0, rot_seed=5)):
+            with pytest.raises(K.KashinError) as e:
+                call()
+            assert e.value.status == K.KASHIN_E_UNSUPPORTED_N
+        torch.cuda.synchronize()
+
+
 def test_zero_and_cube_vertex_rows():
     """A zero row stays zero; a row a*s (s in {-1,1}^N) is all u after one step (T11)."""
     n, k = 512, 4
@@ -470,14 +607,16 @@ def test_zero_and_cube_vertex_rows():
 
 # ----------------------------------------------------------------------------- full-size workloads, sampled rows
 def _sample_rows(w, count, rng):
+    """Row 0, the last row, the three rows of largest ||w||_inf, then random rows up to `count`."""
     m = w.shape[0]
-    pick = {0, m - 1, int(np.argmax(np.abs(w.astype(np.float32)).max(axis=1)))}
+    mx = np.abs(w.astype(np.float32)).max(axis=1)
+    pick = {0, m - 1} | {int(i) for i in np.argsort(mx)[-3:]}
     while len(pick) < min(count, m):
         pick.add(int(rng.integers(0, m)))
     return sorted(pick)
 
 
-WL = [("gauss512", None), ("opt125m", 4), ("llama7b", 3), ("pythia7b", 2)]
+WL_ROWS = {"gauss512": None, "opt125m": 8, "llama7b": 8, "pythia7b": 8}  # sampled rows per matrix (None: all)
 
 
 def _load_matrix(wl, layer, idx):
@@ -494,10 +633,11 @@ def _load_matrix(wl, layer, idx):
     return w, wd, plan, out
 
 
-def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded):
+def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded, lloyd=0):
     """Replay sampled rows (all rows if per_matrix is None) of matrix idx, already quantised in
     full in the benchmark's launch configuration, against the oracle: factors, reconstruction,
-    centres and codes.  Returns (code mismatches, codes compared)."""
+    centres (closed form from the replayed step sizes, then `lloyd` passes of the oracle's Lloyd on
+    the replayed factors) and codes.  Returns (code mismatches, codes compared)."""
     spec = wl.matrices[idx]
     w, wd, plan, (cu, cv, ce) = loaded
     seed = synth.sign_seed(wl, layer, idx)
@@ -505,13 +645,16 @@ def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded):
     signs, _, u_tr, v_tr = pu.gpu_trace(plan, wd, rows, wl.iters)
     eps = ref.sign_mask(spec.n, seed)
     w64 = w[rows].astype(np.float64)
-    res = pu.replay_parity(w64, eps, wl.iters, signs, u_tr, v_tr)
-    _say(f"{key}/L{layer}/{spec.name} N={spec.n} rows={len(rows)}: du={res['du'].max():.2e} "
-         f"dv={res['dv'].max():.2e} rec={res['rec'].max():.2e} direct ok={res['direct_frac_ok']:.2f}")
+    res = pu.replay_parity(w64, eps, wl.iters, signs, u_tr, v_tr, direct=spec.n < 11008)
+    _say(f"{key}/L{layer}/{spec.name} N={spec.n} rows={len(rows)} lloyd={lloyd}: du={res['du'].max():.2e} "
+         f"dv={res['dv'].max():.2e} rec={res['rec'].max():.2e} direct ok={res['direct_frac_ok']}")
     pu.assert_replay_ok(res, f"{key}/L{layer}/{spec.name}")
     rep = res["rep"]
     qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
     qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+    if lloyd:
+        qu = ref.lloyd(rep["u"], qu, lloyd)
+        qv = ref.lloyd(rep["vhat"], qv, lloyd)
     ce_s = ce.cpu().numpy()[rows]
     pu.assert_centres_close(ce_s[:, 0], qu)
     pu.assert_centres_close(ce_s[:, 1], qv)
@@ -524,7 +667,7 @@ def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded):
     return mu + mv, 2 * tot
 
 
-def _quantize_grouped(loaded):
+def _quantize_grouped(loaded, lloyd=0):
     """One kashin_quantize_grouped call per vector length (at most 16 matrices each), as the
     benchmark launches them."""
     by_n = {}
@@ -532,34 +675,58 @@ def _quantize_grouped(loaded):
         by_n.setdefault(plan.n, []).append((plan, wd) + out)
     for items in by_n.values():
         for c0 in range(0, len(items), 16):
-            K.kashin_quantize_grouped(items[c0:c0 + 16], 0)
+            K.kashin_quantize_grouped(items[c0:c0 + 16], lloyd)
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("key,per_matrix", WL)
-def test_workload_sampled_rows(key, per_matrix):
-    """Every matrix of the workload (first layer) quantised in full by the grouped launches the
-    benchmark times; sampled rows replayed."""
+_WL_CACHE = {}
+
+
+def _workload_quantised(key, lloyd=0):
+    """Every matrix of the workload's first layer, quantised in full by the grouped launches the
+    benchmark times; kept for the tests of one workload (one workload's buffers at a time)."""
+    ck = (key, lloyd)
+    if ck not in _WL_CACHE:
+        _WL_CACHE.clear()
+        torch.cuda.empty_cache()
+        wl = synth.WORKLOADS[key]
+        loaded = [_load_matrix(wl, 0, idx) for idx in range(len(wl.matrices))]
+        _quantize_grouped(loaded, lloyd)
+        _WL_CACHE[ck] = loaded
+    return _WL_CACHE[ck]
+
+
+WL_MATRICES = [(key, i) for key in WL_ROWS for i in range(len(synth.WORKLOADS[key].matrices))]
+
+
+@pytest.mark.parametrize("key,idx", WL_MATRICES)
+def test_workload_matrix_sampled_rows(key, idx):
+    """Every matrix of every single-layer workload (each with its own sign mask), quantised in full
+    by the grouped launches of the benchmark; row 0, the last row, the three largest-||w||_inf rows
+    and random rows (8 per matrix; all rows of the 256-row matrix) replayed against the oracle."""
     wl = synth.WORKLOADS[key]
-    rng = np.random.default_rng(11)
-    loaded = [_load_matrix(wl, 0, idx) for idx in range(len(wl.matrices))]
-    _quantize_grouped(loaded)
-    total_m = total_codes = 0
-    for idx, spec in enumerate(wl.matrices):
-        if key == "llama7b" and spec.name in ("k_proj", "v_proj", "up_proj"):
-            continue  # same shapes as q_proj / gate_proj; keeps the test within its time budget
-        if key == "pythia7b" and spec.name in ("qkv_1", "qkv_2", "dense"):
-            continue
-        mm, tot = _check_matrix(key, wl, 0, idx, per_matrix, rng, loaded[idx])
-        total_m += mm
-        total_codes += tot
-    _say(f"{key}: code mismatches {total_m} of {total_codes}")
-    assert total_m <= max(1, int(1e-4 * total_codes))
+    loaded = _workload_quantised(key)
+    mm, tot = _check_matrix(key, wl, 0, idx, WL_ROWS[key], np.random.default_rng(11 + idx), loaded[idx])
+    _say(f"{key}/{wl.matrices[idx].name}: code mismatches {mm} of {tot}")
+    assert mm <= max(1, int(1e-4 * tot))
+
+
+@pytest.mark.parametrize("idx", [0, 4, 6])
+def test_llama7b_layer_lloyd2(idx):
+    """The llama7b layer quantised with two Lloyd passes (all seven matrices, grouped launches):
+    sampled rows against the oracle's replayed decomposition followed by the oracle's Lloyd passes
+    on the replayed factors (centres and codes)."""
+    wl = synth.WORKLOADS["llama7b"]
+    loaded = _workload_quantised("llama7b", lloyd=2)
+    mm, tot = _check_matrix("llama7b", wl, 0, idx, 5, np.random.default_rng(40 + idx), loaded[idx], lloyd=2)
+    _say(f"llama7b lloyd=2 {wl.matrices[idx].name}: code mismatches {mm} of {tot}")
+    assert mm <= max(1, int(1e-4 * tot))
 
 
 def test_stack_first_and_last_layer():
     """The 32-layer stack (Student-t(3), outlier columns x50, k = 40): q_proj and down_proj of
-    the first and the last layer quantised in full, two sampled rows each replayed."""
+    the first and the last layer quantised in full, four sampled rows each replayed."""
+    _WL_CACHE.clear()
     wl = synth.WORKLOADS["llama7b_stack"]
     rng = np.random.default_rng(12)
     names = [s.name for s in wl.matrices]
@@ -568,7 +735,7 @@ def test_stack_first_and_last_layer():
         for name in ("q_proj", "down_proj"):
             loaded = _load_matrix(wl, layer, names.index(name))
             _quantize_grouped([loaded])
-            mm, tot = _check_matrix("llama7b_stack", wl, layer, names.index(name), 2, rng, loaded)
+            mm, tot = _check_matrix("llama7b_stack", wl, layer, names.index(name), 4, rng, loaded)
             total_m += mm
             total_codes += tot
     _say(f"llama7b_stack: code mismatches {total_m} of {total_codes}")
@@ -728,8 +895,7 @@ def test_optq_pipeline_stepwise():
     record = []
     cu, cv, ce, q_t = optq.optq_quantize(plan, w_t, pu.to_dev(h), chunk, record=record)
     torch.cuda.synchronize()
-    hd = h + 0.01 * np.mean(np.diag(h)) * np.eye(d_in)
-    u = np.linalg.cholesky(np.linalg.inv(hd)).T
+    u = ref.compensation_factor(h)  # the oracle's damping (0.01 mean diag H) and factor
     scale = np.abs(w).max()
     for snap in record:
         c0, c1 = snap["c0"], snap["c1"]
@@ -758,6 +924,65 @@ def test_optq_pipeline_stepwise():
             assert err <= 1e-5
             wc_rest = got
     del plan
+
+
+def _replaying_quantiser(plan, eps, k, record, codes_u, codes_v, n):
+    """Column quantiser for ref.optq_kashin that follows the GPU run chunk by chunk: the oracle
+    decomposes its own columns in float64, taking the GPU's sign only on entries within the tie
+    band (the GPU's record of the same chunk, traced again), and takes the GPU's code only where its
+    own decision lies within the boundary band; everything else is the oracle's."""
+    by_c0 = {snap["c0"]: snap for snap in record}
+
+    def quantiser(cols, c0):
+        snap = by_c0[c0]
+        nr = cols.shape[0]
+        signs, _, _, _ = pu.gpu_trace(plan, snap["w_chunk"], list(range(nr)), k)
+        winf = np.abs(cols).max(axis=1)
+        d = ref.decompose(cols, eps, k, replay_signs=signs, tau=pu.TAU_REL * winf)
+        assert not d["replay_outside"].any(), f"chunk {c0}: a sign decision outside the tie band differs"
+        cu, cv, ce = ref.cluster2bit(d["u"], d["vhat"], d["cstep"], 0, decide_dtype=np.float32)
+        gu = pu.unpack(codes_u[c0:c0 + nr].cpu().numpy(), n)
+        gv = pu.unpack(codes_v[c0:c0 + nr].cpu().numpy(), n)
+        for mine, gpu, x, q in ((cu, gu, d["u"], ce[:, 0]), (cv, gv, d["vhat"], ce[:, 1])):
+            mism = mine != gpu
+            if mism.any():
+                dist = pu.boundary_distance(x, q) / winf[:, None]
+                assert dist[mism].max() <= pu.TOL_CODE_BOUNDARY, f"chunk {c0}: a code differs away from a boundary"
+                mine[mism] = gpu[mism]
+        return ref.reconstruct(cu, cv, ce, eps), (ref.pack2bit(cu), ref.pack2bit(cv), ce)
+
+    return quantiser
+
+
+@pytest.mark.parametrize("chunk,exact", [(32, False), (32, True), (1, False)])
+def test_optq_pipeline_end_to_end(chunk, exact):
+    """The whole compensated pipeline against ref.optq_kashin: the final dequantised Q and the
+    compensated W.  The chunk form at chunk 32 against the oracle's chunk form at 32; the exact form
+    (columns one at a time inside chunks of 32, lazy trailing update) and chunk 1 against the
+    oracle's per-column form (eq. optq_update column by column).  The oracle follows the GPU only at
+    near-ties (see _replaying_quantiser)."""
+    from paper_2609_11687_amd import optq
+
+    d_out, d_in, k = 512, 96, 20
+    rng = np.random.default_rng(23)
+    w = _rows(rng, d_in, d_out, "t4")  # W^T
+    h = ref.synthetic_hessian(d_in, 300, 10, outlier_cols=3, outlier_scale=8.0)
+    seed = 43
+    eps = ref.sign_mask(d_out, seed)
+    plan = K.kashin_plan(d_out, seed, k)
+    w_t = pu.to_dev(w)
+    record = []
+    cu, cv, ce, q_t = optq.optq_quantize(plan, w_t, pu.to_dev(h), chunk, record=record, exact=exact)
+    torch.cuda.synchronize()
+    oracle_chunk = 1 if (exact or chunk == 1) else chunk
+    q_ref, w_ref, _ = ref.optq_kashin(w.T.astype(np.float64), h, eps, k, oracle_chunk,
+                                      quantiser=_replaying_quantiser(plan, eps, k, record, cu, cv, d_out))
+    scale = np.abs(w).max()
+    dq = np.abs(q_t.cpu().numpy().astype(np.float64) - q_ref.T).max() / scale
+    dw = np.abs(w_t.cpu().numpy().astype(np.float64) - w_ref.T).max() / scale
+    _say(f"optq end to end chunk={chunk} exact={exact}: max |Q - Q_ref| = {dq:.2e}, max |W - W_ref| = {dw:.2e} "
+         f"(of max |W|)")
+    assert dq <= 1e-4 and dw <= 1e-4
 
 
 @pytest.mark.parametrize("n", [172, 512, 768, 4096, 11008])
