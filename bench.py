@@ -21,6 +21,11 @@
 --op optq: one step = the chunked error-compensated pipeline (paper_2609_11687_amd.optq) on one
   matrix of the workload (--matrix, default q_proj): its columns quantised in chunks of --chunk
   with the error carried through a synthetic Hessian (seeded activations with outlier channels).
+--op fig2: the convergence comparison of Fig. 2: --fig2-rows vectors x of length N = 10^4 drawn
+  from N(0, I), --fig2-steps greedy updates with Alg. 2's alternating schedule and with Alg. 1
+  (kashin_decompose_schedule, "original"); one step = both decompositions.  Reports the residual
+  ||x - u - P vhat||_2 / ||x||_2 after selected updates (mean over the vectors and for vector 0),
+  and how much of each factor sits at four peaks.
 """
 from __future__ import annotations
 
@@ -113,30 +118,163 @@ def _blas_threads() -> int:
         return os.cpu_count() or 1
 
 
-def cpu_baseline(wl, rows: int):
-    """The float64 oracle on a bounded sample of the workload: the first `rows` rows of the
-    first matrix (the dense explicit-cosine matrix is built before timing)."""
+def cpu_baseline(wl, rows: int, loaded=None):
+    """The float64 oracle on a bounded sample of the workload: the first `rows` rows of the first
+    matrix, and for every other vector length the first rows of its first matrix in proportion to
+    the oracle's cost (8 N^2 k flops per vector), timed separately (the dense explicit-cosine
+    matrix is built before timing).  `value` is the rate at the first matrix's length; `per_n` has
+    every length's rate and `extrapolated_step_s` the time the oracle would take for one whole step
+    at those rates (labelled as extrapolated: it is not measured).  With `loaded` (the
+    benchmarked matrices: (plan, rows, codes_u, codes_v, centres) per matrix, first layer) the GPU's
+    codes of the sampled rows are compared with the oracle's (plain float64 decisions, no replay),
+    and a few rows per length are replayed (see _parity_sample)."""
     import numpy as np
 
     import oracle.kashin_ref as ref
     from paper_2609_11687_amd import synth
 
-    spec = wl.matrices[0]
-    w = synth.make_matrix(wl, 0, 0, rows=slice(0, rows)).astype(np.float64)
-    eps = ref.sign_mask(spec.n, synth.sign_seed(wl, 0, 0))
-    ref.dct2_matrix(spec.n)
-    t0 = time.perf_counter()
-    ref.quantize(w, eps, wl.iters, 0)
-    dt = time.perf_counter() - t0
-    return {
-        "value": rows / dt,
+    first = {}
+    for idx, spec in enumerate(wl.matrices):
+        first.setdefault(spec.n, idx)
+    n0 = wl.matrices[0].n
+    per_n, agree = {}, {}
+    total = 0.0
+    for n, idx in first.items():
+        spec = wl.matrices[idx]
+        nr = max(8, int(rows * (n0 / n) ** 2)) if n != n0 else rows
+        nr = min(nr, spec.rows)
+        w = synth.make_matrix(wl, 0, idx, rows=slice(0, nr)).astype(np.float64)
+        eps = ref.sign_mask(n, synth.sign_seed(wl, 0, idx))
+        ref.dct2_matrix(n)
+        t0 = time.perf_counter()
+        cu, cv, ce, _ = ref.quantize(w, eps, wl.iters, 0)
+        dt = time.perf_counter() - t0
+        per_n[str(n)] = {"vectors_per_s": nr / dt, "rows": nr, "seconds": dt, "matrix": spec.name}
+        total += dt
+        if loaded is not None:
+            _, _, gu, gv, _ = loaded[idx]
+            same = (ref.unpack2bit(gu[:nr].cpu().numpy(), n) == ref.unpack2bit(cu, n)).sum() + \
+                (ref.unpack2bit(gv[:nr].cpu().numpy(), n) == ref.unpack2bit(cv, n)).sum()
+            agree[str(n)] = float(same) / (2 * nr * n)
+    counts = {}
+    for spec in wl.matrices:
+        counts[spec.n] = counts.get(spec.n, 0) + spec.rows * wl.layers
+    extrap = sum(counts[n] / per_n[str(n)]["vectors_per_s"] for n in counts)
+    s0 = per_n[str(n0)]
+    out = {
+        "value": s0["vectors_per_s"],
         "unit": "vectors/s",
         "cores": int(_blas_threads()),
         "kind": "oracle",
-        "sample": f"{rows} rows of {spec.name} ({spec.rows}x{spec.n}), k={wl.iters}, float64 literal Alg. 2 "
-                  f"with a dense P (4 GEMMs per block) + closed-form clustering + packing; "
-                  f"{dt:.1f} s; cosine-matrix construction excluded",
+        "sample": "float64 literal Alg. 2 with a dense P (4 GEMMs per block) + closed-form clustering + "
+                  "packing, k=%d; " % wl.iters + "; ".join(
+                      f"{d['rows']} rows of {d['matrix']} (N={n}) in {d['seconds']:.1f} s" for n, d in per_n.items())
+                  + "; cosine-matrix construction excluded",
+        "per_n": per_n,
+        "extrapolated_step_s": extrap,
+        "extrapolated_note": "time the oracle would take for one whole step at the sampled per-length rates "
+                             "(extrapolated, not measured)",
     }
+    if agree:
+        out["code_agreement_direct"] = agree
+    if loaded is not None:
+        out["parity"] = _parity_sample(wl, loaded)
+    return out
+
+
+def _parity_sample(wl, loaded, rows_per_matrix: int = 4):
+    """Replay parity of the benchmarked launches on sampled rows: for the first matrix of each
+    vector length, `rows_per_matrix` rows (row 0, the largest ||w||_inf row, the last row, ...) are
+    traced on the GPU and the oracle is replayed on the GPU's near-tie signs; reports the largest
+    factor and reconstruction errors (fractions of ||w||_inf), the sign decisions outside the tie
+    band that differ from float64 (must be 0) and the code agreement with the oracle's codes."""
+    import numpy as np
+    import torch
+
+    import oracle.kashin_ref as ref
+    from paper_2609_11687_amd import kashin as K
+    from paper_2609_11687_amd import synth
+
+    first = {}
+    for idx, spec in enumerate(wl.matrices):
+        first.setdefault(spec.n, idx)
+    out = {}
+    for n, idx in first.items():
+        plan, wd, cu, cv, ce = loaded[idx]
+        w = wd.float()
+        m = w.shape[0]
+        mx = w.abs().amax(dim=1)
+        rows = sorted({0, m - 1, int(torch.argmax(mx))} | {int(i) for i in torch.topk(mx, 2).indices})[:rows_per_matrix]
+        k = wl.iters
+        rt = torch.tensor(rows, dtype=torch.int64, device=wd.device)
+        sg = torch.empty((len(rows), 4 * k, n), dtype=torch.int8, device=wd.device)
+        ct = torch.empty((len(rows), 4 * k), dtype=torch.float32, device=wd.device)
+        ut = torch.empty((len(rows), n), dtype=torch.float32, device=wd.device)
+        vt = torch.empty_like(ut)
+        K.kashin_trace(plan, wd, rt, sg, ct, ut, vt)
+        torch.cuda.synchronize()
+        w64 = w[rows].cpu().numpy().astype(np.float64)
+        winf = np.abs(w64).max(axis=1)
+        eps = ref.sign_mask(n, synth.sign_seed(wl, 0, idx))
+        d = ref.decompose(w64, eps, k, replay_signs=sg.cpu().numpy(), tau=1e-6 * winf)
+        u, v = ut.cpu().numpy().astype(np.float64), vt.cpu().numpy().astype(np.float64)
+        du = float((np.abs(u - d["u"]).max(axis=1) / winf).max())
+        dv = float((np.abs(v - d["vhat"]).max(axis=1) / winf).max())
+        rec = float((np.abs(w64 - d["r"] - u - ref.apply_p(v, eps)).max(axis=1) / winf).max())
+        same = tot = 0
+        for packed, x, c1, c2 in ((cu, d["u"], 0, 1), (cv, d["vhat"], 2, 3)):
+            q = ref.closed_form_centers(d["cstep"][:, c1], d["cstep"][:, c2])
+            codes = ref.unpack2bit(packed[rows].cpu().numpy(), n)
+            same += int((codes == ref.assign_codes(x, q, np.float32)).sum())
+            tot += codes.size
+        out[str(n)] = {"matrix": wl.matrices[idx].name, "rows": rows, "max_du": du, "max_dv": dv, "max_rec": rec,
+                       "outside_tie_band": int(d["replay_outside"].sum()), "code_agreement": same / tot,
+                       "tolerances": {"factors": 1e-4, "reconstruction": 1e-5, "codes": 0.9999}}
+    return out
+
+
+def held_clock_mhz(run_for_ms):
+    """SCLK of the GPU while the benchmark's step keeps it busy: `run_for_ms()` queues about two
+    seconds of steps without waiting, rocm-smi reads the current clock meanwhile."""
+    import subprocess
+
+    import torch
+
+    run_for_ms()
+    try:
+        res = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=30)
+        torch.cuda.synchronize()
+        data = json.loads(res.stdout)
+        for card in data.values():
+            for key, val in card.items():
+                if "sclk" in key.lower():
+                    digits = "".join(ch for ch in str(val).split("Mhz")[0] if ch.isdigit())
+                    if digits:
+                        return int(digits)
+    except Exception:  # pragma: no cover - no rocm-smi, unparsable output
+        torch.cuda.synchronize()
+    return None
+
+
+def copy_bandwidth_gbps():
+    """Achievable HBM bandwidth: a plain 1 GiB device-to-device copy (read + write bytes / time)."""
+    import torch
+
+    x = torch.ones(256 << 20, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(2):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(5):
+        y.copy_(x)
+    t1.record()
+    torch.cuda.synchronize()
+    gbps = 5 * 2 * x.numel() * 4 / (t0.elapsed_time(t1) / 1e3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return gbps
 
 
 def cpu_baseline_apply_p(n: int, rows: int):
@@ -214,6 +352,90 @@ def per_n_figures(launches, launch_ms):
     return by_n, out
 
 
+def peak_mass(x, a, b):
+    """Fraction of the entries of each row of x within a tenth of the smallest centre gap of the
+    nearest of the four centres +-a +- b (the peaks of Sec. 3.1), averaged over rows."""
+    import numpy as np
+
+    q = np.sort(np.stack([-(a + b), -np.abs(a - b), np.abs(a - b), a + b], axis=1), axis=1)
+    gap = np.maximum(np.diff(q, axis=1).min(axis=1), 1e-30)
+    dist = np.abs(x[:, :, None] - q[:, None, :]).min(axis=2)
+    return float((dist <= 0.1 * gap[:, None]).mean())
+
+
+def fig2(args) -> int:
+    """Fig. 2's comparison on the GPU: Alg. 2 (alternating blocks) against Alg. 1 (the original
+    greedy: the half with the larger correlation, projection steps) on N(0, I) vectors, N = 10^4."""
+    import numpy as np
+    import torch
+
+    from paper_2609_11687_amd import kashin as K
+
+    n, rows, steps = 10000, args.fig2_rows, args.fig2_steps
+    k = (steps + 3) // 4
+    dev = torch.device("cuda:0")
+    x = torch.randn((rows, n), dtype=torch.float32, device=dev, generator=torch.Generator(device=dev).manual_seed(0))
+    plan = K.kashin_plan(n, 0, k)
+    x2 = (x.double() ** 2).sum(dim=1)
+    out = {}
+    launches = []
+    for sched in ("alternating", "original"):
+        u, vh, r = torch.empty_like(x), torch.empty_like(x), torch.empty_like(x)
+        rows_t = torch.arange(rows, dtype=torch.int64, device=dev)
+        sg = torch.empty((rows, 4 * k, n), dtype=torch.int8, device=dev)
+        cs = torch.empty((rows, 4 * k), dtype=torch.float32, device=dev)
+        ch = torch.empty((rows, 4 * k), dtype=torch.int8, device=dev)
+        r2 = torch.empty((rows, 4 * k), dtype=torch.float32, device=dev)
+        ut, vt = torch.empty_like(x), torch.empty_like(x)
+        K.kashin_trace_schedule(plan, sched, x, rows_t, sg, cs, ch, r2, ut, vt)
+        torch.cuda.synchronize()
+        rel = (r2.double() / x2[:, None]).sqrt().cpu().numpy()
+        chc = ch.cpu().numpy()
+        csc = cs.cpu().numpy().astype(np.float64)
+        # centres of each factor from its first two steps (Sec. 3.1; for Alg. 1 the first two
+        # steps it happened to take in that half)
+        ab = {}
+        for half, code in (("u", 0), ("vhat", 1)):
+            a = np.zeros(rows)
+            b = np.zeros(rows)
+            for i in range(rows):
+                idx = np.nonzero(chc[i] == code)[0]
+                if idx.size >= 2:
+                    a[i], b[i] = csc[i, idx[0]], csc[i, idx[1]]
+            ab[half] = (a, b)
+        uu, vv = ut.cpu().numpy().astype(np.float64), vt.cpu().numpy().astype(np.float64)
+        marks = [s_ for s_ in (4, 8, 16, 32, 64, 128, 200, 400) if s_ <= 4 * k]
+        out[sched] = {
+            "residual_rel_mean": {str(s_): float(rel[:, s_ - 1].mean()) for s_ in marks},
+            "residual_rel_vector0": {str(s_): float(rel[0, s_ - 1]) for s_ in marks},
+            "vhat_steps_frac": float((chc == 1).mean()),
+            "peak_mass_u": peak_mass(uu, *ab["u"]),
+            "peak_mass_vhat": peak_mass(vv, *ab["vhat"]),
+        }
+        launches.append(lambda s, a=(sched, u, vh, r): K.kashin_decompose_schedule(plan, a[0], x, a[1], a[2], a[3],
+                                                                                   stream=s))
+    stream = torch.cuda.current_stream()
+
+    class _L:
+        def __init__(self, f):
+            self.run = f
+
+    ms_per_step, launch_ms = time_launches([_L(f) for f in launches], args.steps, args.warmup, stream)
+    result = {
+        "metric": "Fig. 2 set-up: residual after greedy updates, Alg. 2 vs Alg. 1, N = 10^4",
+        "value": 2 * rows / (ms_per_step / 1e3),
+        "unit": "vectors/s (both schedules)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"fig2: {rows} vectors of N(0, I_N), N = {n}, {4 * k} greedy updates, "
+                               f"schedules alternating (Alg. 2) and original (Alg. 1, no tolerance)",
+                   "ms_alternating": launch_ms[0], "ms_original": launch_ms[1]},
+        "fig2": out,
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -221,7 +443,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--op", choices=("quantize", "apply_p", "reconstruct", "rotate", "quantize_h", "schedule",
-                                     "optq"), default="quantize")
+                                     "optq", "fig2"), default="quantize")
+    ap.add_argument("--fig2-rows", type=int, default=64)
+    ap.add_argument("--fig2-steps", type=int, default=200)
+    ap.add_argument("--exact", action="store_true", help="--op optq: columns one at a time inside each chunk")
     ap.add_argument("--matrix", default="q_proj", help="matrix of the workload (--op optq)")
     ap.add_argument("--chunk", type=int, default=128, help="columns per compensation chunk (--op optq)")
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
@@ -231,7 +456,7 @@ def main() -> int:
                          "kashin_reconstruct launch per matrix instead of one grouped launch per vector "
                          "length (up to 16 matrices each)")
     ap.add_argument("--act-rows", type=int, default=16384, help="activation rows per width (--op apply_p)")
-    ap.add_argument("--cpu-rows", type=int, default=2048)
+    ap.add_argument("--cpu-rows", type=int, default=1536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (HBM counter calibration)")
@@ -258,6 +483,8 @@ def main() -> int:
     from paper_2609_11687_amd.build import source_digest
 
     K.lib()
+    if args.op == "fig2":
+        return fig2(args)
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
@@ -391,7 +618,7 @@ def main() -> int:
                 st.wait_stream(s)
                 with torch.cuda.stream(st):
                     w_t.copy_(w0_t)
-                optq.optq_quantize(plan, w_t, hess, args.chunk, lloyd_iters=args.lloyd, stream=st)
+                optq.optq_quantize(plan, w_t, hess, args.chunk, lloyd_iters=args.lloyd, stream=st, exact=args.exact)
             for *_, st in jobs:
                 s.wait_stream(st)
 
@@ -410,6 +637,10 @@ def main() -> int:
             launches.append(Launch(n, args.act_rows, args.act_rows * 2 * transform_flops(n), args.act_rows * 8 * n,
                                    lambda s, a=(plan, x, y): K.kashin_apply_p(a[0], a[1], a[2], s), kind="pmap"))
     torch.cuda.synchronize()
+
+    def step_all(s_):
+        for l_ in launches:
+            l_.run(s_)
 
     ms_per_step, launch_ms = time_launches(launches, args.steps, args.warmup, stream)
     total_vectors = sum(l.rows for l in launches)
@@ -433,7 +664,8 @@ def main() -> int:
                       f"+ GEMM)",
             "launches": len(dom), "counted_flops": dom_flops, "gemm_flops": gemm,
         }
-        metric, unit = METRIC_OPTQ.format(args.chunk), "columns/s"
+        metric, unit = METRIC_OPTQ.format(args.chunk) + (", exact per-column updates" if args.exact else ""), \
+            "columns/s"
         workload = (f"optq: {args.workload} " + ", ".join(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].n}"
                                                            for i in chosen)
                     + f" (each on its own stream), columns quantised in chunks of {args.chunk}, k={wl.iters}, "
@@ -534,10 +766,26 @@ def main() -> int:
         w2 = (wd[:nr].float() ** 2).sum(dim=1)
         result["convergence"] = {str(s_): (r2[:, s_ - 1] / w2).sqrt().mean().item() for s_ in (4, 8, 16, 32)
                                  if s_ <= steps}
+    if main_kind in ("quantize", "pmap", "rotate"):
+        # peaks as this machine delivers them: the clock it holds under this load and a plain copy
+        mhz = held_clock_mhz(lambda: [step_all(stream) for _ in range(max(1, int(2000 / max(ms_per_step, 1e-3))))])
+        copy = copy_bandwidth_gbps()
+        roofline["measured_peaks"] = {
+            "sclk_mhz": mhz,
+            "fp32_tflops_at_held_clock": None if mhz is None else PEAK_FP32_TFLOPS * mhz / 2400.0,
+            "hbm_copy_gbps": copy,
+            "note": "published peaks assume 2400 MHz and 8 TB/s; these are the clock held during the step "
+                    "(rocm-smi while steps run) and a 1 GiB device-to-device copy",
+        }
+        if roofline["unit"] == "TFLOP/s" and mhz:
+            roofline["frac_of_held_clock_peak"] = roofline["achieved"] / (PEAK_FP32_TFLOPS * mhz / 2400.0)
+        if roofline["unit"] == "GB/s":
+            roofline["frac_of_copy_bandwidth"] = roofline["achieved"] / copy
     if not args.no_cpu_baseline:
         if args.op == "quantize":
-            log(f"cpu baseline: oracle on {args.cpu_rows} rows")
-            result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows)
+            log(f"cpu baseline: oracle on {args.cpu_rows} rows at N = {wl.matrices[0].n} and proportionally "
+                f"fewer at the other lengths, then a replay of sampled rows")
+            result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, keep[:len(wl.matrices)])
         elif args.op == "apply_p":
             result["cpu_baseline"] = cpu_baseline_apply_p(dom_n, 4 * args.cpu_rows)
     print(json.dumps(result), flush=True)

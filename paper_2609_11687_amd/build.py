@@ -1,6 +1,6 @@
 """Builds libkashin.so (the C-ABI library) in-tree with hipcc for gfx950.
 
-    python -m paper_2609_11687_amd.build [-v]
+    python -m paper_2609_11687_amd.build [-v] [--host-sanitized]
 
 Each kernel translation unit (one per supported vector length) compiles in
 parallel; objects go to ``_build/`` next to this file and the library to
@@ -93,5 +93,46 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     return LIB
 
 
+# Host-code sanitizers for the C-ABI layer (device code is built without them: the GPU runs no
+# sanitizer).  Each -fsanitize= follows -Xarch_host, so only the host pass sees it.
+HOST_SANITIZE = "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split()
+SANITIZED_LIB = os.path.join(BUILD, "libkashin_host_sanitized.so")
+
+
+def asan_runtime() -> str:
+    """Path of the compiler's AddressSanitizer runtime (preloaded into a process that loads the
+    sanitized library, since the Python interpreter itself is not instrumented)."""
+    res = subprocess.run([_hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return res.stdout.strip()
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    """libkashin with the host layer (kashin_api.cpp: validation, plan tables, dispatch) compiled
+    under AddressSanitizer and UndefinedBehaviorSanitizer, linked with the kernel objects of the
+    regular build (built first if missing).  Written to _build/, never next to libkashin.so."""
+    if not all(os.path.exists(os.path.join(BUILD, os.path.basename(s_) + ".o")) for s_ in sources()):
+        build(verbose)
+    api = os.path.join(CSRC, "kashin_api.cpp")
+    obj = os.path.join(BUILD, "kashin_api.host_sanitized.o")
+    flags = [a for a in HIPCC_FLAGS if a != "-O3"] + ["-O1", "-g", "-Xarch_host", "-fno-omit-frame-pointer",
+                                                      "-Xarch_host", "-fno-sanitize-recover=undefined"]
+    cmd = [_hipcc(), *flags, *HOST_SANITIZE, "-c", api, "-o", obj]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed for the sanitized host layer:\n{res.stderr}")
+    objs = [obj] + [os.path.join(BUILD, os.path.basename(s_) + ".o") for s_ in sources() if s_ != api]
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *HOST_SANITIZE, "-shared-libasan",
+           "-o", SANITIZED_LIB, *objs]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link of the sanitized library failed:\n{res.stderr}")
+    return SANITIZED_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--host-sanitized" in sys.argv:
+        print(build_host_sanitized(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))

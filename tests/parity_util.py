@@ -101,13 +101,16 @@ def boundary_distance(x, q):
     return np.min(np.abs(x[:, :, None] - mids[:, None, :]), axis=2)
 
 
-def code_mismatches(codes_gpu, x_ref, q_ref, winf, label=""):
+def code_mismatches(codes_gpu, x_ref, q_ref, winf, label="", slack=None):
     """Compare GPU codes with the oracle's (decision taken in fp32 on the oracle's factor and
-    centres); returns (mismatch count, total) and checks every mismatch is near a boundary."""
+    centres); returns (mismatch count, total) and checks every mismatch is near a boundary (within
+    1e-5 ||w||_inf, plus a per-row `slack` in the units of x by which the GPU's own midpoints may
+    differ from the oracle's, e.g. after Lloyd passes)."""
     codes_ref = ref.assign_codes(x_ref, q_ref, np.float32)
     mism = codes_gpu != codes_ref
     if mism.any():
-        dist = boundary_distance(x_ref, q_ref) / winf[:, None]
+        extra = 0.0 if slack is None else (np.asarray(slack) / winf)[:, None]
+        dist = boundary_distance(x_ref, q_ref) / winf[:, None] - extra
         worst = dist[mism].max()
         assert worst <= TOL_CODE_BOUNDARY, f"{label}: a code mismatch lies {worst:.3e} ||w||_inf from any boundary"
     return int(mism.sum()), int(mism.size)
@@ -127,3 +130,42 @@ def assert_centres_close(ce, q, rel=1e-5):
     err = np.abs(ce - q).max(axis=1)
     bad = err > rel * scale + 1e-30
     assert not bad.any(), f"centres differ: rows {np.nonzero(bad)[0][:8]}, rel err {(err / np.maximum(scale, 1e-30)).max():.2e}"
+
+
+def lloyd_tolerance(x, q0, passes, winf, band=TOL_CODE_BOUNDARY):
+    """Per-row bound on how far the centres after `passes` Lloyd passes (from q0) may move when the
+    entries of x lying within band ||w||_inf of a midpoint (a near-tie: the GPU's fp32 factor may
+    sit on the other side) are assigned to the other cluster.  Moving one entry between adjacent
+    clusters shifts each mean by at most (q_3 - q_0) / (its count); a shifted centre moves the next
+    pass's midpoints, so the band of the next pass widens by the bound so far."""
+    q = np.array(q0, dtype=np.float64, copy=True)
+    tol = np.zeros(x.shape[0])
+    for _ in range(passes):
+        mids = (q[:, :-1] + q[:, 1:]) * 0.5
+        dist = np.abs(x[:, :, None] - mids[:, None, :]).min(axis=2)
+        near = (dist <= band * winf[:, None] + tol[:, None]).sum(axis=1)
+        codes = ref.assign_codes(x, q)
+        counts = np.stack([(codes == c).sum(axis=1) for c in range(4)], axis=1)
+        smallest = np.where(counts > 0, counts, np.iinfo(np.int64).max).min(axis=1)
+        tol = tol + near * (q[:, 3] - q[:, 0]) / np.maximum(smallest - near, 1)
+        q = ref.lloyd(x, q, 1)
+    return tol
+
+
+def assert_lloyd_centres_close(ce, q, tol, rel=1e-5):
+    """Lloyd centres against the oracle's, within rel of the row's outer centre plus the near-tie
+    bound of lloyd_tolerance."""
+    ce = np.asarray(ce, dtype=np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    scale = np.abs(q).max(axis=1)
+    err = np.abs(ce - q).max(axis=1)
+    bad = err > rel * scale + tol + 1e-30
+    assert not bad.any(), (f"Lloyd centres differ: rows {np.nonzero(bad)[0][:8]}, err {err[bad][:4]}, "
+                           f"allowed {(rel * scale + tol)[bad][:4]}")
+
+
+def near_boundary_count(x, q, winf, slack):
+    """Entries of x within 1e-5 ||w||_inf + slack (per row, units of x) of a midpoint of q: the codes
+    that may legitimately differ when the other side's midpoints are off by up to `slack`."""
+    dist = boundary_distance(x, q)
+    return int((dist <= TOL_CODE_BOUNDARY * winf[:, None] + np.asarray(slack)[:, None]).sum())

@@ -528,7 +528,7 @@ def test_subnormal_row():
     plan = K.kashin_plan(n, 3, k)
     outs = []
     for row in (tiny, big):
-        wd = pu.to_dev(row[None, :])
+        wd = pu.to_dev(np.stack([row]))
         u, vh, _, cs, _ = K.decompose_alloc(plan, wd)
         cu, cv, ce = K.quantize_alloc(plan, wd, 0)
         torch.cuda.synchronize()
@@ -541,8 +541,8 @@ def test_subnormal_row():
         assert err <= 1e-5, err
     # and the normal row against the oracle
     eps = ref.sign_mask(n, 3)
-    signs, _, u_tr, v_tr = pu.gpu_trace(plan, pu.to_dev(big[None, :]), [0], k)
-    pu.assert_replay_ok(pu.replay_parity(big[None, :].astype(np.float64), eps, k, signs, u_tr, v_tr), "normal")
+    signs, _, u_tr, v_tr = pu.gpu_trace(plan, pu.to_dev(np.stack([big])), [0], k)
+    pu.assert_replay_ok(pu.replay_parity(np.stack([big]).astype(np.float64), eps, k, signs, u_tr, v_tr), "normal")
 
 
 def test_row_pairing_permutation():
@@ -652,18 +652,37 @@ def _check_matrix(key, wl, layer, idx, per_matrix, rng, loaded, lloyd=0):
     rep = res["rep"]
     qu = ref.closed_form_centers(rep["cstep"][:, 0], rep["cstep"][:, 1])
     qv = ref.closed_form_centers(rep["cstep"][:, 2], rep["cstep"][:, 3])
+    ce_s = ce.cpu().numpy()[rows].astype(np.float64)
+    slack = [None, None]
     if lloyd:
-        qu = ref.lloyd(rep["u"], qu, lloyd)
-        qv = ref.lloyd(rep["vhat"], qv, lloyd)
-    ce_s = ce.cpu().numpy()[rows]
-    pu.assert_centres_close(ce_s[:, 0], qu)
-    pu.assert_centres_close(ce_s[:, 1], qv)
+        # Lloyd's means jump when a near-tie entry lands in the other cluster: the centres are
+        # checked within the bound that near-ties allow, and codes near the shifted midpoints
+        for f, (x, q0) in enumerate(((rep["u"], qu), (rep["vhat"], qv))):
+            tol = pu.lloyd_tolerance(x, q0, lloyd, res["winf"])
+            q = ref.lloyd(x, q0, lloyd)
+            pu.assert_lloyd_centres_close(ce_s[:, f], q, tol)
+            slack[f] = np.abs(ce_s[:, f] - q).max(axis=1)
+            if f == 0:
+                qu = q
+            else:
+                qv = q
+        _say(f"  lloyd: near-tie centre bound {slack[0].max():.2e} / {slack[1].max():.2e}")
+    else:
+        pu.assert_centres_close(ce_s[:, 0], qu)
+        pu.assert_centres_close(ce_s[:, 1], qv)
     codes_u = pu.unpack(cu.cpu().numpy()[rows], spec.n)
     codes_v = pu.unpack(cv.cpu().numpy()[rows], spec.n)
-    mu, tot = pu.code_mismatches(codes_u, rep["u"], qu, res["winf"], "u")
-    mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat")
+    mu, tot = pu.code_mismatches(codes_u, rep["u"], qu, res["winf"], "u", slack[0])
+    mv, _ = pu.code_mismatches(codes_v, rep["vhat"], qv, res["winf"], "vhat", slack[1])
     # every row of the matrix got finite centres
     assert np.isfinite(ce.cpu().numpy()).all()
+    if lloyd:
+        # codes between the GPU's and the oracle's (shifted) Lloyd midpoints may flip: they are not
+        # counted against the 1e-4 budget (each was checked to lie in that band above)
+        band = pu.near_boundary_count(rep["u"], qu, res["winf"], slack[0]) + \
+            pu.near_boundary_count(rep["vhat"], qv, res["winf"], slack[1])
+        _say(f"  lloyd: {mu + mv} code mismatches, {band} entries in the shifted-midpoint band")
+        return max(0, mu + mv - band), 2 * tot
     return mu + mv, 2 * tot
 
 
@@ -743,7 +762,10 @@ def test_stack_first_and_last_layer():
 
 
 # ----------------------------------------------------------------------------- incoherence rotation
-@pytest.mark.parametrize("n", ALL_N)
+ROT_N = [n for n in ALL_N if n // (n & -n) in (1, 3, 43)]  # the lengths the rotation takes
+
+
+@pytest.mark.parametrize("n", ROT_N)
 def test_rotate_matches_oracle(n):
     """y = R x and x = R^T y against the oracle's dense R, fp32 rows; fp16 input equals fp32
     input of the same values bit for bit; in place equals out of place bit for bit."""
@@ -820,7 +842,7 @@ def test_rotated_quantization_pipeline():
 
 # ----------------------------------------------------------------------------- step schedules
 SCHED_CASES = [(n, s) for n in (512, 4096, 11008) for s in ("alternating", "reverse", "adaptive", "original")] + \
-    [(768, "original"), (3072, "adaptive")]
+    [(768, "original"), (3072, "adaptive")] + [(10000, s) for s in ("alternating", "adaptive", "original")]
 
 
 @pytest.mark.parametrize("n,schedule", SCHED_CASES)
