@@ -112,8 +112,10 @@ def _rows(w):
     """(m, ldw) of a row-major 2-D tensor whose rows are unit-stride."""
     if w.dim() == 2 and w.shape[0] == 0:  # no rows: strides are arbitrary (torch gives 0 for empty arrays)
         return 0, w.shape[1]
-    if w.dim() != 2 or w.stride(1) != 1:
+    if w.dim() != 2 or (w.stride(1) != 1 and w.shape[1] > 1):
         raise ValueError("expected a 2-D tensor with unit-stride rows")
+    if w.shape[0] == 1:  # one row: its stride is never used (numpy and torch may report 0)
+        return 1, w.shape[1]
     return w.shape[0], w.stride(0)
 
 
