@@ -26,7 +26,8 @@
  *     Results are deterministic run to run; a row's last bits may depend on the
  *     row it is paired with.
  *   - Plans are immutable after creation and may be shared across host threads and
- *     streams.  No entry point other than kashin_plan allocates device memory.
+ *     streams.  No entry point other than kashin_plan (its tables) and kashin_optq_factor (its
+ *     temporaries, freed before it returns) allocates device memory.
  */
 #ifndef KASHIN_H_
 #define KASHIN_H_
@@ -235,6 +236,46 @@ int kashin_reconstruct_rotated(kashin_plan_t plan, uint64_t rot_seed, const uint
 int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, int64_t ldw,
                  const int64_t* rows, int64_t nrows, int8_t* sign_trace, float* c_trace,
                  float* u, float* vhat, void* stream);
+
+/* Error-compensated quantisation (Sec. 5, Fig. 1: the columns of W quantised one after another, each
+ * one's error carried into the columns not yet quantised, eq. optq_update with the 1 % damping of
+ * the Sec. 5 remark).  W (d_out x d_in) is held transposed, w_t = W^T (d_in rows of n = d_out), so a
+ * column of W is a row of w_t.
+ *
+ * kashin_optq_factor: from H (d x d fp32 row-major, leading dimension ldh >= d, symmetric; device),
+ * the upper-triangular U with U^T U = (H + lambda I)^-1, lambda = damp * mean(diag H), and V = U^-1
+ * (v nullable), both d x d float64 row-major (device, caller-owned).  Computed as the lower Cholesky
+ * factor L of J (H + lambda I) J (J reverses the index order: then H + lambda I = V V^T with
+ * V = J L J upper) and its triangular inverse, in float64 (rocSOLVER).  Unlike every other entry
+ * point it allocates temporary device memory (d x d float64 and the solver's workspace) and frees it
+ * before returning, and it synchronises `stream`.  KASHIN_E_INVALID if the damped Hessian is not
+ * positive definite. */
+int kashin_optq_factor(const float* h, int32_t d, int64_t ldh, double damp, double* u, double* v, void* stream);
+
+/* Device workspace bytes kashin_optq_quantize needs for d_in rows of length n in chunks of `chunk`
+ * (an error matrix, chunk x n fp32, and a factor block, chunk x d_in fp32); -1 for bad sizes. */
+int64_t kashin_optq_workspace_bytes(int64_t d_in, int32_t n, int32_t chunk);
+
+/* Quantise rows 0 .. quantize_rows - 1 of w_t (d_in rows, fp32, leading dimension ldw >= n = the
+ * plan's length; device) with error compensation, carrying their errors into every later row of
+ * w_t, which is updated in place (quantize_rows = d_in: the whole matrix; a smaller count lets a
+ * caller resume on the tail, with the factor's trailing block).  u, v: the output of
+ * kashin_optq_factor for d = d_in, leading dimension ldu >= d_in (v may be NULL when exact = 1).
+ * Outputs for the quantised rows (device): codes_u, codes_v rows x ceil(n/4), centers rows x 2 x 4 (as
+ * kashin_quantize), q_t rows x n fp32 (ld n): the dequantised rows (as kashin_reconstruct).
+ *   exact = 0: chunks of `chunk` rows (1 <= chunk <= 128) quantised together; after each chunk c,
+ *              w_t[r] -= (U_cc^-1 U_cr)^T Delta with Delta = w_t[c] - q_t[c] for the later rows r;
+ *              equal to eq. optq_update at chunk = 1.
+ *   exact = 1: rows quantised one at a time; err_i = (w_t[i] - q_t[i]) / U_ii reaches the later rows
+ *              j of its chunk at once (w_t[j] -= U_ij err_i) and the rows after the chunk in one
+ *              product at the chunk's end (w_t[r] -= U_cr^T E): eq. optq_update row by row for any
+ *              chunk size.
+ * work: at least kashin_optq_workspace_bytes(d_in, n, chunk) bytes of device memory (its contents on
+ * entry do not matter).  Allocates nothing; every launch is queued on `stream`. */
+int kashin_optq_quantize(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u, const double* v,
+                         int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact, int32_t lloyd_iters,
+                         uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t, void* work,
+                         int64_t work_bytes, void* stream);
 
 /* Static text for a status code. */
 const char* kashin_status_string(int status);

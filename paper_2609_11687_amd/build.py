@@ -35,6 +35,10 @@ HIPCC_FLAGS = [
 ]
 
 
+# the Cholesky factorisation and triangular inverse of the compensation factor (kashin_optq_factor)
+LINK_LIBS = ["-L/opt/rocm/lib", "-lrocsolver", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"]
+
+
 def _hipcc() -> str:
     for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -44,7 +48,7 @@ def _hipcc() -> str:
 
 def sources() -> list[str]:
     srcs = [os.path.join(CSRC, "kashin_api.cpp"), os.path.join(CSRC, "kashin_dispatch.hip"),
-            os.path.join(CSRC, "kashin_rotate.hip")]
+            os.path.join(CSRC, "kashin_rotate.hip"), os.path.join(CSRC, "kashin_optq.hip")]
     srcs += sorted(glob.glob(os.path.join(CSRC, "kashin_n*.hip")))
     return srcs
 
@@ -83,7 +87,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), order))
     tmp = LIB + ".tmp"
-    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs, *LINK_LIBS]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -124,7 +128,7 @@ def build_host_sanitized(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed for the sanitized host layer:\n{res.stderr}")
     objs = [obj] + [os.path.join(BUILD, os.path.basename(s_) + ".o") for s_ in sources() if s_ != api]
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *HOST_SANITIZE, "-shared-libasan",
-           "-o", SANITIZED_LIB, *objs]
+           "-o", SANITIZED_LIB, *objs, *LINK_LIBS]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link of the sanitized library failed:\n{res.stderr}")

@@ -588,6 +588,103 @@ int kashin_cluster2bit(kashin_plan_t plan, const float* u, const float* vhat, co
   return ok();
 }
 
+int kashin_optq_factor(const float* h, int32_t d, int64_t ldh, double damp, double* u, double* v, void* stream) {
+  if (d < 1) return fail(KASHIN_E_INVALID, "d must be >= 1 (got %d)", d);
+  if (ldh < d) return fail(KASHIN_E_INVALID, "ldh (%lld) < d (%d)", (long long)ldh, d);
+  if (!(damp >= 0.0) || !(damp <= 1e30)) return fail(KASHIN_E_INVALID, "damp must be finite and >= 0");
+  if (!h || !u) return fail(KASHIN_E_INVALID, "h and u must be non-null");
+  int info = 0;
+  const hipError_t e = kashin::optq_factor_device(h, d, ldh, damp, u, v, static_cast<hipStream_t>(stream), &info);
+  if (e != hipSuccess) return hip_fail(e, "compensation factor");
+  if (info > 0)
+    return fail(KASHIN_E_INVALID, "the damped Hessian is not positive definite (leading minor %d)", info);
+  if (info < 0) return fail(KASHIN_E_INVALID, "the Cholesky factor is singular (diagonal entry %d)", -info);
+  return ok();
+}
+
+int64_t kashin_optq_workspace_bytes(int64_t d_in, int32_t n, int32_t chunk) {
+  if (d_in < 0 || n < 1 || chunk < 1) return -1;
+  return kashin::optq_workspace_bytes(d_in, n, chunk);
+}
+
+namespace {
+// The compensation loop of kashin_optq_quantize with workspace `work` (at least
+// optq_workspace_bytes(d_in, n, chunk) bytes of device memory).
+int optq_run(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u, const double* v,
+             int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact, int32_t lloyd_iters, uint8_t* codes_u,
+             uint8_t* codes_v, float* centers, float* q_t, char* work, void* stream) {
+  const int n = plan->n;
+  const int64_t nb = (n + 3) / 4;
+  const int64_t ce = std::min<int64_t>(chunk, d_in);
+  float* e_buf = reinterpret_cast<float*>(work);
+  float* m_buf = reinterpret_cast<float*>(work + (((ce * n * 4) + 255) & ~int64_t(255)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int64_t c0 = 0; c0 < quantize_rows; c0 += chunk) {
+    const int64_t c1 = std::min<int64_t>(c0 + chunk, quantize_rows);
+    const int rows = static_cast<int>(c1 - c0);
+    const int64_t steps = exact ? rows : 1;  // exact: one column at a time
+    for (int64_t t = 0; t < steps; ++t) {
+      const int64_t r0 = exact ? c0 + t : c0, r1 = exact ? r0 + 1 : c1;
+      int st = kashin_quantize(plan, w_t + r0 * ldw, KASHIN_F32, r1 - r0, ldw, lloyd_iters, codes_u + r0 * nb,
+                               codes_v + r0 * nb, centers + r0 * 8, stream);
+      if (st) return st;
+      st = kashin_reconstruct(plan, codes_u + r0 * nb, codes_v + r0 * nb, centers + r0 * 8, r1 - r0, q_t + r0 * n, n,
+                              stream);
+      if (st) return st;
+      if (exact) {
+        // err_i = (w_i - q_i) / U_ii into row i - c0 of the chunk's error matrix, then carried to
+        // the chunk's later columns
+        hipError_t e = kashin::optq_error(w_t, ldw, q_t, n, r0, 1, u, ldu, e_buf + (r0 - c0) * n, s);
+        if (e == hipSuccess) e = kashin::optq_rank1(w_t, ldw, n, r0, r0 + 1, c1, u, ldu, e_buf + (r0 - c0) * n, s);
+        if (e != hipSuccess) return hip_fail(e, "compensation kernels");
+      }
+    }
+    const int64_t rest = d_in - c1;
+    if (rest <= 0) continue;
+    hipError_t e = hipSuccess;
+    if (!exact) e = kashin::optq_error(w_t, ldw, q_t, n, c0, rows, nullptr, 0, e_buf, s);  // Delta
+    if (e == hipSuccess) e = kashin::optq_chunk_factor(u, v, ldu, c0, rows, c1, rest, exact != 0, m_buf, s);
+    if (e == hipSuccess) e = kashin::optq_update(w_t + c1 * ldw, ldw, m_buf, e_buf, rows, rest, n, s);
+    if (e != hipSuccess) return hip_fail(e, "compensation kernels");
+  }
+  return ok();
+}
+
+int optq_check(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u, const double* v,
+               int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact, int32_t lloyd_iters,
+               uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t) {
+  int st = check_common(plan, d_in);
+  if (st) return st;
+  if (ldu < d_in) return fail(KASHIN_E_INVALID, "ldu (%lld) < d_in (%lld)", (long long)ldu, (long long)d_in);
+  if (quantize_rows < 0 || quantize_rows > d_in)
+    return fail(KASHIN_E_INVALID, "quantize_rows must be in [0, d_in] (got %lld)", (long long)quantize_rows);
+  if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
+  if (chunk < 1 || chunk > kashin::kOptqMaxChunk)
+    return fail(KASHIN_E_INVALID, "chunk must be in [1, %d] (got %d)", kashin::kOptqMaxChunk, chunk);
+  if (exact != 0 && exact != 1) return fail(KASHIN_E_INVALID, "exact must be 0 or 1");
+  if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
+  if (d_in > 0 && (!w_t || !u || !codes_u || !codes_v || !centers || !q_t))
+    return fail(KASHIN_E_INVALID, "w_t, u, codes, centers and q_t must be non-null");
+  if (d_in > 0 && !exact && !v) return fail(KASHIN_E_INVALID, "the chunk form needs v");
+  return KASHIN_OK;
+}
+}  // namespace
+
+int kashin_optq_quantize(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u, const double* v,
+                         int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact, int32_t lloyd_iters,
+                         uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t, void* work,
+                         int64_t work_bytes, void* stream) {
+  int st = optq_check(plan, w_t, d_in, ldw, u, v, ldu, quantize_rows, chunk, exact, lloyd_iters, codes_u, codes_v,
+                      centers, q_t);
+  if (st) return st;
+  if (quantize_rows == 0) return ok();
+  const int64_t need = kashin::optq_workspace_bytes(d_in, plan->n, chunk);
+  if (!work || work_bytes < need)
+    return fail(KASHIN_E_INVALID, "work must hold %lld bytes (got %lld)", (long long)need, (long long)work_bytes);
+  return optq_run(plan, w_t, d_in, ldw, u, v, ldu, quantize_rows, chunk, exact, lloyd_iters, codes_u, codes_v,
+                  centers, q_t, static_cast<char*>(work), stream);
+}
+
 const char* kashin_status_string(int status) {
   switch (status) {
     case KASHIN_OK: return "ok";

@@ -144,6 +144,23 @@ bool supported_n(int n);
 hipError_t launch_pair(int n, const KArgs& a, int64_t grid, hipStream_t stream);
 hipError_t launch_cluster(const ClusterArgs& a, hipStream_t stream);
 
+// Error-compensated quantisation (kashin_optq.hip).  optq_factor_device: U (upper, U^T U =
+// (H + lambda I)^-1, lambda = damp mean(diag H)) and, if v != null, V = U^-1, both d x d float64
+// row-major; allocates and frees its temporaries and synchronises `stream`; *info != 0 when the
+// damped Hessian is not positive definite (> 0) or its factor singular (< 0).
+hipError_t optq_factor_device(const float* h, int d, int64_t ldh, double damp, double* u, double* v,
+                              hipStream_t stream, int* info);
+constexpr int kOptqMaxChunk = 128;
+int64_t optq_workspace_bytes(int64_t d_in, int n, int chunk);
+hipError_t optq_error(const float* w, int64_t ldw, const float* q, int n, int64_t row0, int rows, const double* u,
+                      int64_t ldu, float* e, hipStream_t s);
+hipError_t optq_rank1(float* w, int64_t ldw, int n, int64_t i, int64_t j0, int64_t j1, const double* u, int64_t ldu,
+                      const float* err, hipStream_t s);
+hipError_t optq_chunk_factor(const double* u, const double* v, int64_t ld, int64_t c0, int rows, int64_t c1,
+                             int64_t rest, bool exact, float* m, hipStream_t s);
+hipError_t optq_update(float* w_rest, int64_t ldw, const float* m, const float* e, int rows, int64_t rest, int n,
+                       hipStream_t s);
+
 // Incoherence rotation of rows (kashin_rotate.hip).
 bool rotate_supported_n(int n);
 hipError_t launch_rotate(int n, uint64_t seed, bool inverse, const void* x, int dtype, int64_t ldx, float* y,

@@ -25,8 +25,8 @@ EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
     "kashin_quantize", "kashin_quantize_grouped", "kashin_reconstruct_grouped", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
-    "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_status_string",
-    "kashin_last_error",
+    "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_optq_factor",
+    "kashin_optq_workspace_bytes", "kashin_optq_quantize", "kashin_status_string", "kashin_last_error",
 )
 SCHEDULES = {"alternating": 0, "reverse": 1, "adaptive": 2, "original": 3}
 
@@ -68,11 +68,15 @@ def lib() -> ctypes.CDLL:
         "kashin_decompose_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, vp, vp, vp],
         "kashin_trace_schedule": [vp, i32, ctypes.c_float, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp],
         "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
+        "kashin_optq_factor": [vp, i32, i64, ctypes.c_double, vp, vp, vp],
+        "kashin_optq_quantize": [vp, vp, i64, i64, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, i64, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    L.kashin_optq_workspace_bytes.argtypes = [i64, i32, i32]
+    L.kashin_optq_workspace_bytes.restype = i64
     L.kashin_status_string.argtypes = [ctypes.c_int]
     L.kashin_status_string.restype = ctypes.c_char_p
     L.kashin_last_error.argtypes = []
@@ -386,6 +390,61 @@ def kashin_trace(plan, w, rows, sign_trace, c_trace, u, vhat, stream=None):
     _need(plan, vhat, (nr, plan.n), torch.float32, "vhat")
     _check(lib().kashin_trace(plan.handle, _ptr(w), _dtype_code(w), m, ldw, _ptr(rows), rows.numel(),
                               _ptr(sign_trace), _ptr(c_trace), _ptr(u), _ptr(vhat), _stream(stream)))
+
+
+def kashin_optq_factor(h, u, v=None, damp=0.01, stream=None):
+    """U (upper, U^T U = (H + damp mean(diag H) I)^-1) and V = U^-1 into u, v (d x d float64,
+    contiguous, on H's device); H is d x d fp32 with unit-stride rows."""
+    import torch
+    d, ldh = _rows(h)
+    if h.shape[1] != d or h.dtype != torch.float32:
+        raise ValueError("h must be a square fp32 matrix")
+    _need(None, u, (d, d), torch.float64, "u")
+    _need(None, v, (d, d), torch.float64, "v", nullable=True)
+    _on_plan_device(None, h, "h")
+    _check(lib().kashin_optq_factor(_ptr(h), d, ldh, damp, _ptr(u), _ptr(v), _stream(stream)))
+
+
+def kashin_optq_workspace_bytes(d_in: int, n: int, chunk: int) -> int:
+    return int(lib().kashin_optq_workspace_bytes(d_in, n, chunk))
+
+
+def _need_square_rows(plan, t, d, name, nullable=False):
+    """A d x d float64 matrix (or a d x d block of a larger one) with unit-stride rows."""
+    import torch
+    if t is None:
+        if nullable:
+            return None
+        raise ValueError(f"{name} is required")
+    if t.dtype != torch.float64 or t.dim() != 2 or tuple(t.shape) != (d, d) or (d > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name} must be a {d} x {d} float64 matrix with unit-stride rows")
+    if d:
+        _on_plan_device(plan, t, name)
+    return t.stride(0) if d > 1 else max(d, 1)
+
+
+def kashin_optq_quantize(plan, w_t, u, v, chunk, exact, lloyd_iters, codes_u, codes_v, centers, q_t, work,
+                         quantize_rows=None, stream=None):
+    """Error-compensated quantisation of the rows of w_t (d_in x n fp32, updated in place) with the
+    factor (u, v) of kashin_optq_factor (or trailing blocks of it: any leading dimension); the first
+    `quantize_rows` rows (default all) are quantised.  work: a uint8 device buffer of at least
+    kashin_optq_workspace_bytes(d_in, n, chunk) bytes."""
+    import torch
+    d_in, ldw = _need_rows(plan, w_t, plan.n, "w_t", (torch.float32,))
+    qr = d_in if quantize_rows is None else quantize_rows
+    ldu = _need_square_rows(plan, u, d_in, "u")
+    ldv = _need_square_rows(plan, v, d_in, "v", nullable=bool(exact))
+    if ldv is not None and ldv != ldu:
+        raise ValueError("u and v must have the same leading dimension")
+    _need_codes(plan, qr, codes_u, codes_v, centers)
+    _need(plan, q_t, (qr, plan.n), torch.float32, "q_t")
+    if work.dtype != torch.uint8 or work.dim() != 1 or (work.numel() and not work.is_contiguous()):
+        raise ValueError("work must be a contiguous 1-D uint8 tensor")
+    if work.numel():
+        _on_plan_device(plan, work, "work")
+    _check(lib().kashin_optq_quantize(plan.handle, _ptr(w_t), d_in, ldw, _ptr(u), _ptr(v), ldu, qr, chunk,
+                                      1 if exact else 0, lloyd_iters, _ptr(codes_u), _ptr(codes_v), _ptr(centers),
+                                      _ptr(q_t), _ptr(work), work.numel(), _stream(stream)))
 
 
 # ----------------------------------------------------------------------------- allocating helpers

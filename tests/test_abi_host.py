@@ -248,3 +248,20 @@ def test_binding_checks_buffers_before_calling():
     # all layouts right: the call reaches the library, which rejects the null plan
     with pytest.raises(K.KashinError):
         K.kashin_quantize(plan, w0, 0, cu, cv, ce, stream=0)
+
+
+def test_optq_entry_points_validate_before_device():
+    """The compensation entry points check sizes, factors, chunk, workspace and the plan on the host."""
+    L = K.lib()
+    buf = ctypes.c_void_p(0x1000)
+    f = ctypes.c_double
+    assert L.kashin_optq_factor(buf, 0, 0, f(0.01), buf, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_optq_factor(buf, 4, 3, f(0.01), buf, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_optq_factor(buf, 4, 4, f(-1.0), buf, None, None) == K.KASHIN_E_INVALID
+    assert L.kashin_optq_factor(None, 4, 4, f(0.01), buf, None, None) == K.KASHIN_E_INVALID
+    assert K.kashin_optq_workspace_bytes(-1, 512, 8) == -1
+    assert K.kashin_optq_workspace_bytes(100, 512, 8) == ((8 * 512 * 4 + 255) // 256) * 256 + 8 * 100 * 4
+    fake = ctypes.c_void_p(0x1234)
+    args = (buf, 4, 512, buf, buf, 4, 4, 8, 0, 0, buf, buf, buf, buf, buf, 1 << 20, None)
+    assert L.kashin_optq_quantize(fake, *args) == K.KASHIN_E_INVALID
+    assert "plan" in L.kashin_last_error().decode()

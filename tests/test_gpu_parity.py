@@ -948,6 +948,26 @@ def test_optq_pipeline_stepwise():
     del plan
 
 
+@pytest.mark.parametrize("d,outliers", [(1, 0), (96, 3), (512, 4), (4096, 8)])
+def test_optq_factor_matches_oracle(d, outliers):
+    """kashin_optq_factor (rocSOLVER Cholesky of the exchange-flipped damped Hessian and its triangular
+    inverse, float64) against the oracle's factor of the inverse: U upper with U^T U = (H + lambda
+    I)^-1, lambda = 0.01 mean(diag H), and V = U^-1."""
+    from paper_2609_11687_amd import optq
+
+    h = ref.synthetic_hessian(d, 2 * d + 8, d, outlier_cols=outliers, outlier_scale=20.0).astype(np.float32)
+    u, v = optq.compensation_factor(pu.to_dev(h))
+    torch.cuda.synchronize()
+    u_ref = ref.compensation_factor(h.astype(np.float64))
+    ug, vg = u.cpu().numpy(), v.cpu().numpy()
+    err_u = np.abs(ug - u_ref).max() / np.abs(u_ref).max()
+    err_v = np.abs(vg @ ug - np.eye(d)).max()
+    _say(f"optq factor d={d}: max |U - U_ref| / max |U_ref| = {err_u:.2e}, max |V U - I| = {err_v:.2e}")
+    assert err_u <= 1e-9
+    assert err_v <= 1e-9
+    assert np.all(np.tril(ug, -1) == 0) and np.all(np.diag(ug) > 0)
+
+
 def _replaying_quantiser(plan, eps, k, record, codes_u, codes_v, n):
     """Column quantiser for ref.optq_kashin that follows the GPU run chunk by chunk: the oracle
     decomposes its own columns in float64, taking the GPU's sign only on entries within the tie
