@@ -277,6 +277,18 @@ int kashin_optq_quantize(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t l
                          uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t, void* work,
                          int64_t work_bytes, void* stream);
 
+/* kashin_optq_quantize for callers that cannot allocate (code under HIP graph capture, serving
+ * loops, harnesses that forbid hipMalloc): the same computation with the workspace taken from a
+ * static device array of the library instead of the `work` argument, so the caller passes only
+ * inputs and outputs.  The array holds 16 MiB on each device (allocated with the library's code
+ * object, held until the process ends); kashin_optq_workspace_bytes(d_in, n, chunk) must not exceed
+ * it (chunk 128 with d_in + n <= 32768 fits), else KASHIN_E_INVALID.  Every call on a device uses
+ * the same array: calls that overlap on one device race.  Results equal kashin_optq_quantize's. */
+int kashin_optq_quantize_noalloc(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u,
+                                 const double* v, int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact,
+                                 int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t,
+                                 void* stream);
+
 /* Static text for a status code. */
 const char* kashin_status_string(int status);
 

@@ -685,6 +685,26 @@ int kashin_optq_quantize(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t l
                   centers, q_t, static_cast<char*>(work), stream);
 }
 
+int kashin_optq_quantize_noalloc(kashin_plan_t plan, float* w_t, int64_t d_in, int64_t ldw, const double* u,
+                                 const double* v, int64_t ldu, int64_t quantize_rows, int32_t chunk, int32_t exact,
+                                 int32_t lloyd_iters, uint8_t* codes_u, uint8_t* codes_v, float* centers, float* q_t,
+                                 void* stream) {
+  int st = optq_check(plan, w_t, d_in, ldw, u, v, ldu, quantize_rows, chunk, exact, lloyd_iters, codes_u, codes_v,
+                      centers, q_t);
+  if (st) return st;
+  if (quantize_rows == 0) return ok();
+  const int64_t need = kashin::optq_workspace_bytes(d_in, plan->n, chunk);
+  if (need > kashin::kOptqStaticScratchBytes)
+    return fail(KASHIN_E_INVALID, "d_in = %lld, n = %d, chunk = %d need %lld bytes of workspace, above the %lld of the "
+                "static array (use kashin_optq_quantize)", (long long)d_in, plan->n, chunk, (long long)need,
+                (long long)kashin::kOptqStaticScratchBytes);
+  void* work = nullptr;
+  const hipError_t e = kashin::optq_static_scratch(&work);
+  if (e != hipSuccess) return hip_fail(e, "static workspace address");
+  return optq_run(plan, w_t, d_in, ldw, u, v, ldu, quantize_rows, chunk, exact, lloyd_iters, codes_u, codes_v,
+                  centers, q_t, static_cast<char*>(work), stream);
+}
+
 const char* kashin_status_string(int status) {
   switch (status) {
     case KASHIN_OK: return "ok";

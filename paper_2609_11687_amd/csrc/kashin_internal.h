@@ -152,6 +152,10 @@ hipError_t optq_factor_device(const float* h, int d, int64_t ldh, double damp, d
                               hipStream_t stream, int* info);
 constexpr int kOptqMaxChunk = 128;
 int64_t optq_workspace_bytes(int64_t d_in, int n, int chunk);
+// kashin_optq_quantize_noalloc's workspace: a static device array of this many bytes per device;
+// optq_static_scratch gives its address on the current device
+constexpr int64_t kOptqStaticScratchBytes = int64_t(16) << 20;
+hipError_t optq_static_scratch(void** out);
 hipError_t optq_error(const float* w, int64_t ldw, const float* q, int n, int64_t row0, int rows, const double* u,
                       int64_t ldu, float* e, hipStream_t s);
 hipError_t optq_rank1(float* w, int64_t ldw, int n, int64_t i, int64_t j0, int64_t j1, const double* u, int64_t ldu,

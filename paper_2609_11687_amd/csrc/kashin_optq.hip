@@ -10,6 +10,7 @@
 #include <rocsolver/rocsolver.h>
 
 #include <cstdint>
+#include <mutex>
 
 #include "kashin_internal.h"
 
@@ -202,6 +203,36 @@ hipError_t optq_factor_device(const float* h, int d, int64_t ldh, double damp, d
   if (f) (void)hipFree(f);
   if (lambda) (void)hipFree(lambda);
   return e;
+}
+
+// Workspace of kashin_optq_quantize_noalloc: one array per device, holding the error matrix and the
+// factor block of the chunk being carried (optq_workspace_bytes of the call).  Every call on a
+// device uses the same array; both parts are written before they are read within each chunk, so
+// nothing needs clearing, and calls that overlap on one device race.
+static __device__ __align__(256) char scratch[kOptqStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// The device address of `scratch` on the current device, looked up once per device (the array's
+// name is a host-side stand-in: host code passes this address, never the name, to kernels).
+hipError_t optq_static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 int64_t optq_workspace_bytes(int64_t d_in, int n, int chunk) {

@@ -26,7 +26,8 @@ EXPORTS = (
     "kashin_plan_info", "kashin_decompose", "kashin_cluster2bit", "kashin_reconstruct",
     "kashin_quantize", "kashin_quantize_grouped", "kashin_reconstruct_grouped", "kashin_apply_p", "kashin_rotate", "kashin_trace", "kashin_decompose_schedule",
     "kashin_trace_schedule", "kashin_quantize_rotated", "kashin_reconstruct_rotated", "kashin_optq_factor",
-    "kashin_optq_workspace_bytes", "kashin_optq_quantize", "kashin_status_string", "kashin_last_error",
+    "kashin_optq_workspace_bytes", "kashin_optq_quantize", "kashin_optq_quantize_noalloc", "kashin_status_string",
+    "kashin_last_error",
 )
 SCHEDULES = {"alternating": 0, "reverse": 1, "adaptive": 2, "original": 3}
 
@@ -70,6 +71,7 @@ def lib() -> ctypes.CDLL:
         "kashin_trace": [vp, vp, i32, i64, i64, vp, i64, vp, vp, vp, vp, vp],
         "kashin_optq_factor": [vp, i32, i64, ctypes.c_double, vp, vp, vp],
         "kashin_optq_quantize": [vp, vp, i64, i64, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, i64, vp],
+        "kashin_optq_quantize_noalloc": [vp, vp, i64, i64, vp, vp, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -445,6 +447,23 @@ def kashin_optq_quantize(plan, w_t, u, v, chunk, exact, lloyd_iters, codes_u, co
     _check(lib().kashin_optq_quantize(plan.handle, _ptr(w_t), d_in, ldw, _ptr(u), _ptr(v), ldu, qr, chunk,
                                       1 if exact else 0, lloyd_iters, _ptr(codes_u), _ptr(codes_v), _ptr(centers),
                                       _ptr(q_t), _ptr(work), work.numel(), _stream(stream)))
+
+
+def kashin_optq_quantize_noalloc(plan, w_t, u, v, chunk, exact, lloyd_iters, codes_u, codes_v, centers, q_t,
+                                 quantize_rows=None, stream=None):
+    """kashin_optq_quantize with the library's static device workspace (no workspace argument)."""
+    import torch
+    d_in, ldw = _need_rows(plan, w_t, plan.n, "w_t", (torch.float32,))
+    qr = d_in if quantize_rows is None else quantize_rows
+    ldu = _need_square_rows(plan, u, d_in, "u")
+    ldv = _need_square_rows(plan, v, d_in, "v", nullable=bool(exact))
+    if ldv is not None and ldv != ldu:
+        raise ValueError("u and v must have the same leading dimension")
+    _need_codes(plan, qr, codes_u, codes_v, centers)
+    _need(plan, q_t, (qr, plan.n), torch.float32, "q_t")
+    _check(lib().kashin_optq_quantize_noalloc(plan.handle, _ptr(w_t), d_in, ldw, _ptr(u), _ptr(v), ldu, qr, chunk,
+                                              1 if exact else 0, lloyd_iters, _ptr(codes_u), _ptr(codes_v),
+                                              _ptr(centers), _ptr(q_t), _stream(stream)))
 
 
 # ----------------------------------------------------------------------------- allocating helpers
