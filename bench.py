@@ -341,7 +341,7 @@ def per_n_figures(launches, launch_ms):
     out = {}
     for n, d in sorted(by_n.items()):
         s = d["ms"] / 1e3
-        out[str(n)] = {
+        out[str(n) if n else "mixed lengths"] = {
             "vectors_per_s": d["vectors"] / s,
             "counted_tflops": d["flops"] / s / 1e12,
             "valu_frac": d["flops"] / s / 1e12 / PEAK_FP32_TFLOPS,
@@ -361,6 +361,23 @@ def peak_mass(x, a, b):
     gap = np.maximum(np.diff(q, axis=1).min(axis=1), 1e-30)
     dist = np.abs(x[:, :, None] - q[:, None, :]).min(axis=2)
     return float((dist <= 0.1 * gap[:, None]).mean())
+
+
+def histogram_modes(x, bins=48, prominence=0.1):
+    """Per row of x: the number of modes of its density, counted as the peaks of a `bins`-bin
+    histogram over [-max|x|, max|x|] (smoothed with weights 1, 2, 1) that rise at least
+    `prominence` times the tallest bin above the deeper of the valleys around them."""
+    import numpy as np
+    from scipy.signal import find_peaks
+
+    out = []
+    for row in x:
+        lim = float(np.abs(row).max()) or 1.0
+        h, _ = np.histogram(row, bins=bins, range=(-lim, lim))
+        hs = np.convolve(np.concatenate([[0], h, [0]]), [0.25, 0.5, 0.25], mode="same")
+        peaks, _ = find_peaks(np.concatenate([[0], hs, [0]]), prominence=prominence * hs.max())
+        out.append(len(peaks))
+    return np.array(out)
 
 
 def fig2(args) -> int:
@@ -403,6 +420,7 @@ def fig2(args) -> int:
                 if idx.size >= 2:
                     a[i], b[i] = csc[i, idx[0]], csc[i, idx[1]]
             ab[half] = (a, b)
+        # u and v-hat: Fig. 2's densities are those of u_k and of U v_k = v-hat (x = u_k + v_k)
         uu, vv = ut.cpu().numpy().astype(np.float64), vt.cpu().numpy().astype(np.float64)
         marks = [s_ for s_ in (4, 8, 16, 32, 64, 128, 200, 400) if s_ <= 4 * k]
         out[sched] = {
@@ -411,6 +429,8 @@ def fig2(args) -> int:
             "vhat_steps_frac": float((chc == 1).mean()),
             "peak_mass_u": peak_mass(uu, *ab["u"]),
             "peak_mass_vhat": peak_mass(vv, *ab["vhat"]),
+            "modes_u": np.bincount(histogram_modes(uu), minlength=6).tolist(),
+            "modes_vhat": np.bincount(histogram_modes(vv), minlength=6).tolist(),
         }
         launches.append(lambda s, a=(sched, u, vh, r): K.kashin_decompose_schedule(plan, a[0], x, a[1], a[2], a[3],
                                                                                    stream=s))
@@ -612,6 +632,8 @@ def main() -> int:
         # timing, as the Hessian itself: it stays alive for every step, so no stream ever reads a
         # factor whose memory the allocator could hand out again
         factors, factor_ms = {}, {}
+        optq.compensation_factor(torch.eye(64, device=dev), want_v=True)  # rocSOLVER's start-up, untimed
+        torch.cuda.synchronize()
         for d_in, hess in hess_by_din.items():
             t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             t0e.record()
@@ -635,7 +657,9 @@ def main() -> int:
             for *_, st in jobs:
                 s.wait_stream(st)
 
-        d_out = jobs[0][1].shape[1]
+        # one launch covers every matrix: its length is the matrices' common d_out, else 0 (mixed)
+        d_outs = {j[1].shape[1] for j in jobs}
+        d_out = d_outs.pop() if len(d_outs) == 1 else 0
         cols = sum(j[1].shape[0] for j in jobs)
         flops = sum(j[1].shape[0] * counted_flops_per_vector(j[1].shape[1], wl.iters) for j in jobs) + gemm
         launches.append(Launch(d_out, cols, flops, sum(j[1].numel() * 12 for j in jobs), run_optq, kind="optq"))
