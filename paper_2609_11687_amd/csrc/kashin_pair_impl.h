@@ -422,6 +422,37 @@ __device__ __forceinline__ void block_sum(float (&v)[K], float* red, int& slot) 
   }
 }
 
+// block_sum for many values over many waves: the workgroup's per-wave partials are summed by the
+// lanes of one DPP row (lane w holds wave w's partial; a quad, half-row and row fold, the same in
+// every wave), so K values cost K registers after the barrier rather than K x (waves), which
+// block_sum's unrolled reads need all at once.  A fixed order again, but another one.
+template <int T, int K>
+__device__ __forceinline__ void block_sum_lanes(float (&v)[K], float* red, int& slot) {
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
+  if constexpr (T > 64) {
+    constexpr int NW = (T + 63) / 64;
+    static_assert(NW <= 16 && K <= 32, "one DPP row of partials, K values per wave in red");
+    float* r = red + (slot & 1) * (NW * 32);
+    ++slot;
+    const int lane = threadIdx.x & 63;
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) r[(threadIdx.x >> 6) * K + k] = v[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      float t = lane < NW ? r[lane * K + k] : 0.f;
+      t += dpp<0xb1>(t);   // quad_perm [1,0,3,2]
+      t += dpp<0x4e>(t);   // quad_perm [2,3,0,1]
+      t += dpp<0x141>(t);  // row_half_mirror
+      t += dpp<0x140>(t);  // row_mirror: every lane of row 0 holds the sum of lanes 0..15
+      v[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(t), 0));
+    }
+  }
+}
+
 template <int T, int K>
 __device__ __forceinline__ void block_max(float (&v)[K], float* red, int& slot) {
 #pragma unroll
@@ -1905,25 +1936,103 @@ __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::W))) vo
   }
 }
 
+// One output of both rows of a pair (the thread's elements given by f(e) as float2: row a in .x,
+// row b in .y) written in row order through the LDS buffer: contiguous 16-byte stores (4-byte
+// ones where a row is not 16-byte aligned) instead of the even/odd order's stride-2 stores, which
+// leave every line half written per instruction.  out_b may be null (no row b to write).  Starts
+// and ends with a barrier, so the buffer is free before and after.
+template <class C, class F>
+__device__ __forceinline__ void store_pair_staged(float2* lds, float* out_a, float* out_b, F&& f) {
+  static_assert(C::N % 4 == 0, "rows staged as float4");
+  float* lf = reinterpret_cast<float*>(lds);
+  const float4* lf4 = reinterpret_cast<const float4*>(lds);
+  __syncthreads();  // earlier readers of the buffer are done
+  for_each_elem<C>([&](int e, int i) {
+    const float2 v = f(e);
+    lf[i] = v.x;
+    lf[C::N + i] = v.y;
+  });
+  __syncthreads();
+  const bool vec_a = (reinterpret_cast<uintptr_t>(out_a) & 15) == 0;
+  const bool vec_b = (reinterpret_cast<uintptr_t>(out_b) & 15) == 0;
+  for (int q = threadIdx.x; q < C::N / 4; q += C::T) {
+    if (out_a != nullptr) {
+      const float4 o = lf4[q];
+      if (vec_a) {
+        reinterpret_cast<float4*>(out_a)[q] = o;
+      } else {
+        out_a[4 * q] = o.x;
+        out_a[4 * q + 1] = o.y;
+        out_a[4 * q + 2] = o.z;
+        out_a[4 * q + 3] = o.w;
+      }
+    }
+    if (out_b != nullptr) {
+      const float4 o = lf4[C::N / 4 + q];
+      if (vec_b) {
+        reinterpret_cast<float4*>(out_b)[q] = o;
+      } else {
+        out_b[4 * q] = o.x;
+        out_b[4 * q + 1] = o.y;
+        out_b[4 * q + 2] = o.z;
+        out_b[4 * q + 3] = o.w;
+      }
+    }
+  }
+  __syncthreads();  // the staged rows are read before the buffer's next writer
+}
+
 // ------------------------------------------------------------------ schedule variants
 // The greedy over Q_N u P Q_N with another step schedule (MODE_SCHEDULE; a.schedule).  Both
 // domains of the residual are kept per row of the pair, rho and z = P rho; a step works in one
 // domain per row (the two rows of a pair may choose differently), and one application of P to
 // the pair's stepped values refreshes the other domain of both rows (P^2 = I).  That is one P
-// per atomic step, twice what the alternating kernel needs, and four live arrays: the
-// register budget is relaxed to two waves per SIMD where the workgroup allows it.
+// per atomic step, twice what the alternating kernel needs; three arrays live across steps (the
+// residual in two domains and vhat).  The register budget is relaxed to two waves per SIMD where
+// the workgroup allows it.
 // With a.rows set, workgroup i decomposes the pair holding row a.rows[i] and records that
 // row's signs, step sizes, choices and ||rho||^2 after every step.
+//
+// Where the workgroup shape caps the registers (more than 512 threads: one workgroup per CU,
+// 168 or 128 VGPRs) the four arrays do not fit; vhat then lives in private memory between its
+// steps (16-byte loads and stores of the whole array at each vhat-step), so that rho, z and the
+// transform's array stay in registers.
 template <class C>
+constexpr bool sched_vh_in_memory() {
+  return (C::T > 512 || C::E >= 32) && C::E % 2 == 0;
+}
+// With a 128-register budget (1024 threads), and on the five-pass shape with 64 values per array
+// (N = 13824), the stepped values wait in private memory too while P runs, so that only the
+// transformed array occupies registers across the transform (the compiler otherwise spills
+// inside the loop there).
+template <class C>
+constexpr bool sched_park() {
+  return sched_vh_in_memory<C>() && ((C::T > 512 && C::W >= 4) || (C::E >= 32 && C::NP >= 5));
+}
+// Where LDS has room beside the transform's buffer (N = 10000, 11008: one element per butterfly
+// thread, B0 = 1), vhat lives there instead, as many of each thread's 2E values as fit (row a's
+// first, then row b's; each thread its own slots, read and written only at vhat-steps), the rest
+// in registers: private memory would be written back to HBM at every vhat-step.
+template <class C>
+constexpr int sched_vh_lds_values() {
+  if constexpr (!sched_vh_in_memory<C>() || sched_park<C>() || C::B0 != 1) {
+    return 0;
+  } else {
+    constexpr int used = (C::LDS + small_tw_total<C>()) * 8 + 2 * C::NW * 32 * 4;
+    constexpr int fit = (160 * 1024 - used) / (4 * C::NB0);
+    return fit < C::E ? 0 : (fit < 2 * C::E ? fit : 2 * C::E);
+  }
+}
+template <class C, bool TRACE>
 __global__ __launch_bounds__(C::T) __attribute__((amdgpu_waves_per_eu(C::T <= 512 ? 2 : C::W))) void
 pair_schedule_kernel(KArgs a, int64_t item0) {
   __shared__ __align__(16) float2 lds[C::LDS + small_tw_total<C>()];
   __shared__ float red[2 * C::NW * 32];
   const int64_t item = item0 + blockIdx.x;
-  const bool tracing = a.rows != nullptr;
+  constexpr bool tracing = TRACE;  // an instance of its own: the trace code costs registers
   int64_t ra;
   int side = 0;
-  if (tracing) {
+  if constexpr (tracing) {
     const int64_t row = a.rows[item];
     if (row < 0 || row >= a.m) return;  // uniform
     ra = row & ~int64_t(1);
@@ -1940,41 +2049,78 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
     if constexpr (RES) apply_P_res<C>(v, lds, rr);
     else apply_P<C>(v, lds, a.tw, a.mid4);
   };
-  float2 rho[C::E], z[C::E], vh[C::E], y[C::E];
-  load_pair<C>(rho, a.w, a.dtype, a.ldw, ra, rb);
+  constexpr int VL = sched_vh_lds_values<C>();  // vhat values per thread in LDS
+  constexpr bool VHL = VL > 0;
+  constexpr bool VHM = sched_vh_in_memory<C>() && !VHL;
+  // The residual of each row in both domains: sv holds it in one domain and y = P sv in the other;
+  // za / zb say which (true: sv holds z = P rho for that row).  A step takes each row's chosen
+  // domain from sv or y, writes the stepped values to sv and transforms them into y, so no select
+  // ever lands on the arrays carried from step to step.
+  float2 sv[C::E], y[C::E], vh[VHM || VHL ? 1 : C::E];
+  float4 vhm[VHM ? C::E / 2 : 1];  // vhat (VHM); a run-time index keeps it in memory
+  // VHL: slot s < VL of thread t at vhl[s * NB0 + t], s = e for row a, E + e for row b; row b's
+  // elements e >= VL - E in vhr
+  __shared__ float vhl[VHL ? VL * C::NB0 : 1];
+  float vhr[VHL && VL < 2 * C::E ? 2 * C::E - VL : 1];
+  const int vt = threadIdx.x;
+  const bool vown = vt < C::NB0;  // threads past the last butterfly hold no elements
+  auto vh_slot = [&](int sl) -> float& { return vhl[sl * C::NB0 + vt]; };
+  constexpr bool PARK = sched_park<C>();
+  float4 park[PARK ? C::E / 2 : 1];  // the stepped values across P (PARK)
+  load_pair<C>(sv, a.w, a.dtype, a.ldw, ra, rb);
   float2 scale, unscale;
   bool bad_a, bad_b;
-  normalise_pair<C>(rho, red, slot, scale, unscale, bad_a, bad_b);
+  normalise_pair<C>(sv, red, slot, scale, unscale, bad_a, bad_b);
 #pragma unroll
-  for (int e = 0; e < C::E; ++e) {
-    z[e] = rho[e];
-    vh[e] = make_float2(0.f, 0.f);
+  for (int e = 0; e < C::E; ++e) y[e] = sv[e];
+  if constexpr (VHM) {
+    const int b = opaque(0);
+#pragma unroll
+    for (int h = 0; h < C::E / 2; ++h) vhm[b + h] = make_float4(0.f, 0.f, 0.f, 0.f);
+  } else if constexpr (VHL) {
+    if (vown) {
+#pragma unroll
+      for (int sl = 0; sl < VL; ++sl) vh_slot(sl) = 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 2 * C::E - VL; ++k) vhr[k] = 0.f;
+  } else {
+#pragma unroll
+    for (int e = 0; e < C::E; ++e) vh[e] = make_float2(0.f, 0.f);
   }
-  applyP(z);
+  applyP(y);
+  bool za = false, zb = false;
   const int steps = 4 * a.iters;
   const int sched = a.schedule;
   const float tola = a.tol * scale.x, tolb = a.tol * scale.y;
   const float unsel = side ? unscale.y : unscale.x;
   for (int st = 0; st < steps; ++st) {
-    // l1 and nonzero counts of both domains, ||rho||^2, both rows
-    float v[10];
+    // l1 norms, nonzero counts and squared norms of sv and y, both rows
+    float s12[12];
 #pragma unroll
-    for (int k = 0; k < 10; ++k) v[k] = 0.f;
+    for (int k = 0; k < 12; ++k) s12[k] = 0.f;
 #pragma unroll
     for (int e = 0; e < C::E; ++e) {
-      v[0] += fabsf(rho[e].x);
-      v[1] += fabsf(rho[e].y);
-      v[2] += fabsf(z[e].x);
-      v[3] += fabsf(z[e].y);
-      v[4] += rho[e].x != 0.f ? 1.f : 0.f;
-      v[5] += rho[e].y != 0.f ? 1.f : 0.f;
-      v[6] += z[e].x != 0.f ? 1.f : 0.f;
-      v[7] += z[e].y != 0.f ? 1.f : 0.f;
-      v[8] += rho[e].x * rho[e].x;
-      v[9] += rho[e].y * rho[e].y;
+      s12[0] += fabsf(sv[e].x);
+      s12[1] += fabsf(sv[e].y);
+      s12[2] += fabsf(y[e].x);
+      s12[3] += fabsf(y[e].y);
+      s12[4] += sv[e].x != 0.f ? 1.f : 0.f;
+      s12[5] += sv[e].y != 0.f ? 1.f : 0.f;
+      s12[6] += y[e].x != 0.f ? 1.f : 0.f;
+      s12[7] += y[e].y != 0.f ? 1.f : 0.f;
+      s12[8] += sv[e].x * sv[e].x;
+      s12[9] += sv[e].y * sv[e].y;
+      s12[10] += y[e].x * y[e].x;
+      s12[11] += y[e].y * y[e].y;
     }
-    block_sum<C::T, 10>(v, red, slot);
+    if constexpr (C::NW * 12 > 64) block_sum_lanes<C::T, 12>(s12, red, slot);
+    else block_sum<C::T, 12>(s12, red, slot);
     // threads past the last butterfly hold zeros: they add nothing to the counts above
+    // v: l1 of rho and z, nonzero counts of rho and z, ||rho||^2 (rows a, b in turn)
+    const float v[10] = {za ? s12[2] : s12[0],  zb ? s12[3] : s12[1], za ? s12[0] : s12[2], zb ? s12[1] : s12[3],
+                         za ? s12[6] : s12[4],  zb ? s12[7] : s12[5], za ? s12[4] : s12[6], zb ? s12[5] : s12[7],
+                         za ? s12[10] : s12[8], zb ? s12[11] : s12[9]};
     const int pos = st & 3;
     bool va, vb;  // true: the vhat-half (step on z)
     if (sched == SCHED_ALTERNATING) {
@@ -1993,8 +2139,11 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
     float cb = sched == SCHED_ORIGINAL ? (nzb > 0.f ? l1b / nzb : 0.f) : div_n<C::N>(l1b);
     ca = act_a ? ca : 0.f;
     cb = act_b ? cb : 0.f;
-    if (tracing) {
+    // each row's chosen domain: in sv when it is the domain sv holds, else in y
+    const bool fa = va == za, fb = vb == zb;
+    if constexpr (tracing) {
       const bool vs = side ? vb : va;
+      const bool fs = side ? fb : fa;
       const int tid = opaque(bfly<C>(threadIdx.x));
       int8_t* trs = a.tr_signs + (item * steps + st) * int64_t(C::N);
 #pragma unroll
@@ -2003,7 +2152,7 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
         if (j < C::NB0) {
 #pragma unroll
           for (int r = 0; r < C::R0; ++r) {
-            const float2 xv = vs ? z[i * C::R0 + r] : rho[i * C::R0 + r];
+            const float2 xv = fs ? sv[i * C::R0 + r] : y[i * C::R0 + r];
             trs[orig_index<C::N>(j + r * C::NB0)] = sgn8(side ? xv.y : xv.x);
           }
         }
@@ -2013,71 +2162,139 @@ pair_schedule_kernel(KArgs a, int64_t item0) {
         a.tr_choice[item * steps + st] = (side ? act_b : act_a) ? (vs ? 1 : 0) : -1;
       }
     }
-    // the step, in each row's chosen domain; y collects the stepped values of both rows
+    // vhat += the steps of the rows that step on z (VHM, VHL: the same values, through memory)
+    if constexpr (VHL) {
+      if (va && vown) {
+#pragma unroll
+        for (int e = 0; e < C::E; ++e) vh_slot(e) += sgn_times(fa ? sv[e].x : y[e].x, ca);
+      }
+      if (vb) {
+#pragma unroll
+        for (int e = 0; e < C::E; ++e) {
+          const float d = sgn_times(fb ? sv[e].y : y[e].y, cb);
+          if (C::E + e < VL) {
+            if (vown) vh_slot(C::E + e) += d;
+          } else {
+            vhr[e - (VL - C::E)] += d;
+          }
+        }
+      }
+    }
+    if constexpr (VHM) {
+      if (va || vb) {
+        const int b = opaque(0);
+#pragma unroll
+        for (int h = 0; h < C::E / 2; ++h) {
+          float4 q = vhm[b + h];
+          if (va) {
+            q.x += sgn_times(fa ? sv[2 * h].x : y[2 * h].x, ca);
+            q.z += sgn_times(fa ? sv[2 * h + 1].x : y[2 * h + 1].x, ca);
+          }
+          if (vb) {
+            q.y += sgn_times(fb ? sv[2 * h].y : y[2 * h].y, cb);
+            q.w += sgn_times(fb ? sv[2 * h + 1].y : y[2 * h + 1].y, cb);
+          }
+          vhm[b + h] = q;
+        }
+      }
+    }
+    // the step, in each row's chosen domain; sv collects the stepped values of both rows
 #pragma unroll
     for (int e = 0; e < C::E; ++e) {
-      float xa = va ? z[e].x : rho[e].x;
-      float xb = vb ? z[e].y : rho[e].y;
+      float xa = fa ? sv[e].x : y[e].x;
+      float xb = fb ? sv[e].y : y[e].y;
       const float da = sgn_times(xa, ca), db = sgn_times(xb, cb);
       xa -= da;
       xb -= db;
-      if (va) {
-        vh[e].x += da;
-        z[e].x = xa;
-      } else {
-        rho[e].x = xa;
+      if constexpr (!VHM && !VHL) {
+        if (va) vh[e].x += da;
+        if (vb) vh[e].y += db;
       }
-      if (vb) {
-        vh[e].y += db;
-        z[e].y = xb;
-      } else {
-        rho[e].y = xb;
-      }
-      y[e] = make_float2(xa, xb);
+      sv[e] = make_float2(xa, xb);
+      y[e] = sv[e];
+    }
+    if constexpr (PARK) {
+      const int b = opaque(0);
+#pragma unroll
+      for (int h = 0; h < C::E / 2; ++h)
+        park[b + h] = make_float4(sv[2 * h].x, sv[2 * h].y, sv[2 * h + 1].x, sv[2 * h + 1].y);
     }
     applyP(y);  // the other domain of each row
+    if constexpr (PARK) {
+      const int b = opaque(0);
 #pragma unroll
-    for (int e = 0; e < C::E; ++e) {
-      if (va) rho[e].x = y[e].x;
-      else z[e].x = y[e].x;
-      if (vb) rho[e].y = y[e].y;
-      else z[e].y = y[e].y;
+      for (int h = 0; h < C::E / 2; ++h) {
+        const float4 q = park[b + h];
+        sv[2 * h] = make_float2(q.x, q.y);
+        sv[2 * h + 1] = make_float2(q.z, q.w);
+      }
     }
-    if (tracing) {
+    za = va;
+    zb = vb;
+    if constexpr (tracing) {
       float q[1] = {0.f};
+      const bool zs = side ? zb : za;  // rho of the traced row: y if sv holds its z
 #pragma unroll
-      for (int e = 0; e < C::E; ++e) q[0] += side ? rho[e].y * rho[e].y : rho[e].x * rho[e].x;
+      for (int e = 0; e < C::E; ++e) {
+        const float2 rv = zs ? y[e] : sv[e];
+        q[0] += side ? rv.y * rv.y : rv.x * rv.x;
+      }
       block_sum<C::T, 1>(q, red, slot);
       if (threadIdx.x == 0) a.tr_r2[item * steps + st] = q[0] * unsel * unsel;
     }
   }
-  // u = w - P vhat - r (row reloaded from HBM)
+  // u = w - r - P vhat (row reloaded from HBM), in steps that keep two arrays live: rho of each
+  // row into sv and out to r; then sv = w - rho; then y = P vhat and u = sv - y
   const float qnan = __int_as_float(0x7fc00000);
 #pragma unroll
-  for (int e = 0; e < C::E; ++e) y[e] = vh[e];
-  applyP(y);
-  float2 t[C::E];
-  load_pair<C>(t, a.w, a.dtype, a.ldw, ra, rb);
+  for (int e = 0; e < C::E; ++e) sv[e] = make_float2(za ? y[e].x : sv[e].x, zb ? y[e].y : sv[e].y);
   int64_t oa = ra, ob = rb;
   bool wa = true, wb = rb >= 0;
-  if (tracing) {
+  if constexpr (tracing) {
     wa = side == 0;
     wb = side == 1;
     oa = ob = item;
   }
-  for_each_elem<C>([&](int e, int i) {
-    const float ua = fmaf(t[e].x, scale.x, -rho[e].x) - y[e].x;
-    const float ub = fmaf(t[e].y, scale.y, -rho[e].y) - y[e].y;
-    if (wa) {
-      a.u[oa * C::N + i] = bad_a ? qnan : ua * unscale.x;
-      a.vhat[oa * C::N + i] = bad_a ? qnan : vh[e].x * unscale.x;
-      if (a.r != nullptr) a.r[oa * C::N + i] = bad_a ? qnan : rho[e].x * unscale.x;
+  auto out_rows = [&](float* base, float*& pa, float*& pb) {
+    pa = wa ? base + oa * C::N : nullptr;
+    pb = wb ? base + ob * C::N : nullptr;
+  };
+  float *pa, *pb;
+  if (a.r != nullptr) {
+    out_rows(a.r, pa, pb);
+    store_pair_staged<C>(lds, pa, pb, [&](int e) {
+      return make_float2(bad_a ? qnan : sv[e].x * unscale.x, bad_b ? qnan : sv[e].y * unscale.y);
+    });
+  }
+  {
+    float2 t[C::E];
+    load_pair<C>(t, a.w, a.dtype, a.ldw, ra, rb);
+#pragma unroll
+    for (int e = 0; e < C::E; ++e)
+      sv[e] = make_float2(fmaf(t[e].x, scale.x, -sv[e].x), fmaf(t[e].y, scale.y, -sv[e].y));
+  }
+  auto vhat_at = [&](int e) -> float2 {
+    if constexpr (VHM) {
+      const float4 q = vhm[opaque(0) + e / 2];
+      return (e & 1) ? make_float2(q.z, q.w) : make_float2(q.x, q.y);
+    } else if constexpr (VHL) {
+      const float b = C::E + e < VL ? (vown ? vh_slot(C::E + e) : 0.f) : vhr[e - (VL - C::E)];
+      return make_float2(vown ? vh_slot(e) : 0.f, b);
+    } else {
+      return vh[e];
     }
-    if (wb) {
-      a.u[ob * C::N + i] = bad_b ? qnan : ub * unscale.y;
-      a.vhat[ob * C::N + i] = bad_b ? qnan : vh[e].y * unscale.y;
-      if (a.r != nullptr) a.r[ob * C::N + i] = bad_b ? qnan : rho[e].y * unscale.y;
-    }
+  };
+#pragma unroll
+  for (int e = 0; e < C::E; ++e) y[e] = vhat_at(e);
+  applyP(y);
+  out_rows(a.u, pa, pb);
+  store_pair_staged<C>(lds, pa, pb, [&](int e) {
+    return make_float2(bad_a ? qnan : (sv[e].x - y[e].x) * unscale.x, bad_b ? qnan : (sv[e].y - y[e].y) * unscale.y);
+  });
+  out_rows(a.vhat, pa, pb);
+  store_pair_staged<C>(lds, pa, pb, [&](int e) {
+    const float2 vhe = vhat_at(e);
+    return make_float2(bad_a ? qnan : vhe.x * unscale.x, bad_b ? qnan : vhe.y * unscale.y);
   });
 }
 
@@ -2113,7 +2330,10 @@ hipError_t launch_cfg(const KArgs& a, int64_t grid, hipStream_t s) {
     } else if (a.mode <= MODE_TRACE) {
       hipLaunchKernelGGL((pair_greedy_kernel<C, false, false, false>), gd, bd, 0, s, a, i0);
     } else if (a.mode == MODE_SCHEDULE) {
-      hipLaunchKernelGGL(pair_schedule_kernel<C>, dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
+      if (a.rows != nullptr)
+        hipLaunchKernelGGL((pair_schedule_kernel<C, true>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
+      else
+        hipLaunchKernelGGL((pair_schedule_kernel<C, false>), dim3(static_cast<unsigned>(g)), dim3(C::T), 0, s, a, i0);
     } else {
       // grouped reconstruction: `grid` is the launch's workgroup count (the matrices' shares)
       const int64_t pg = a.ngroup > 0 ? g : (g < kPmapGrid ? g : kPmapGrid);

@@ -898,6 +898,28 @@ def test_schedule_replay_parity(n, schedule):
         assert (gch == -1).any()  # the tolerance stopped some rows
 
 
+@pytest.mark.parametrize("n", [172, 4096, 11008])
+def test_schedule_outputs_unaligned(n):
+    """The schedule kernel writes its outputs in row order through LDS as 16-byte stores where a
+    row is 16-byte aligned and 4-byte stores where it is not: outputs placed one float off
+    alignment equal the aligned ones bit for bit (odd row count: an unpaired last row)."""
+    k, m = 3, 5
+    rng = np.random.default_rng(n + 5)
+    wd = pu.to_dev(_rows(rng, m, n, "t4"))
+    plan = K.kashin_plan(n, 9, k)
+    outs = []
+    for off in (0, 1):
+        flat = torch.full((3, m * n + 4), float("nan"), dtype=torch.float32, device="cuda")
+        u, vh, r = (flat[j, off:off + m * n].view(m, n) for j in range(3))
+        K.kashin_decompose_schedule(plan, "adaptive", wd, u, vh, r)
+        torch.cuda.synchronize()
+        assert not torch.isnan(flat[:, off:off + m * n]).any()
+        assert torch.isnan(flat[:, :off]).all() and torch.isnan(flat[:, off + m * n:]).all()  # nothing outside
+        outs.append([t.cpu().numpy().copy() for t in (u, vh, r)])
+    for a_, b_ in zip(*outs):
+        np.testing.assert_array_equal(a_, b_)
+
+
 # ----------------------------------------------------------------------------- error compensation
 def test_optq_pipeline_stepwise():
     """The chunked error-compensated pipeline, checked chunk by chunk on the GPU's own state:
