@@ -486,6 +486,11 @@ def main() -> int:
         print("bench.py measures one GPU: rows are independent, so a multi-GPU run would shard them "
               "with no communication; only --gpus 1 is supported.", file=sys.stderr)
         return 2
+    if args.op == "optq":
+        # one hardware queue per matrix chain: the runtime's default is four per process, and
+        # chains sharing a queue run one after the other (read when the runtime starts)
+        if int(os.environ.get("GPU_MAX_HW_QUEUES", "4")) < 8:
+            os.environ["GPU_MAX_HW_QUEUES"] = "8"
 
     import torch
 
@@ -623,7 +628,7 @@ def main() -> int:
                 hess_by_din[d_in] = (x.t() @ x) / x.shape[0]
                 del x
             plan = K.kashin_plan(d_out, synth.sign_seed(wl, 0, idx), wl.iters)
-            jobs.append((plan, w0_t, torch.empty_like(w0_t), hess_by_din[d_in], torch.cuda.Stream(dev)))
+            jobs.append((plan, w0_t, torch.empty_like(w0_t), hess_by_din[d_in], None))
             gemm += sum(2.0 * min(args.chunk, d_in - c0) * d_out * (d_in - min(c0 + args.chunk, d_in))
                         for c0 in range(0, d_in, args.chunk))
         keep.append(jobs)
@@ -643,8 +648,19 @@ def main() -> int:
             factor_ms[str(d_in)] = t0e.elapsed_time(t1e)
         keep.append(factors)
 
-        # the longest chain of chunks (the widest d_in) is queued first, so the others overlap it
-        jobs.sort(key=lambda j: -j[1].shape[0])
+        # Each matrix is one chain of dependent chunks, on a stream of its own as long as the
+        # hardware queues last (streams beyond them share queues, and chains on one queue run one
+        # after the other); otherwise longest first onto the least loaded stream (a chain's cost
+        # taken as chunks x vector length).
+        n_streams = min(int(os.environ.get("GPU_MAX_HW_QUEUES", "4")), len(jobs))
+        streams = [torch.cuda.Stream(dev) for _ in range(n_streams)]
+        load = [0.0] * n_streams
+        placed = []
+        for j in sorted(jobs, key=lambda j: -((j[1].shape[0] + args.chunk - 1) // args.chunk) * j[1].shape[1]):
+            k_ = min(range(n_streams), key=lambda i: load[i])
+            load[k_] += ((j[1].shape[0] + args.chunk - 1) // args.chunk) * j[1].shape[1]
+            placed.append(j[:4] + (streams[k_],))
+        jobs = placed
 
         def run_optq(s):
             # every matrix on its own stream, joined back into the timing stream
@@ -706,7 +722,7 @@ def main() -> int:
             "columns/s"
         workload = (f"optq: {args.workload} " + ", ".join(f"{wl.matrices[i].name} {wl.matrices[i].rows}x{wl.matrices[i].n}"
                                                            for i in chosen)
-                    + f" (each on its own stream), columns quantised in chunks of {args.chunk}, k={wl.iters}, "
+                    + f" (chains on {n_streams} streams, {os.environ.get('GPU_MAX_HW_QUEUES')} hardware queues), columns quantised in chunks of {args.chunk}, k={wl.iters}, "
                     f"Hessian of 2 d_in seeded Gaussian activations with 0.1% outlier channels x20")
     elif main_kind == "schedule":
         achieved = dom_flops / dom_s / 1e12

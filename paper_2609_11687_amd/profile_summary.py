@@ -10,7 +10,8 @@ number of dispatches and the average duration.  The four counter databases (one
 plain 256 MiB device copy) give HBM bytes per dispatch: the raw KiB figure times the factor
 that makes the copy's counter read its known size.  The last line of the output,
 `TRAFFIC_JSON {...}`, carries those bytes per (kernel, vector length, workgroups) together with
-the digest of the kernel sources they were taken on.
+the digest of the kernel sources they were taken on.  --sq (repeatable) adds the shader
+counters of `--pmc SQ_...` runs for the pair kernels, with the busy and wait ratios they give.
 """
 from __future__ import annotations
 
@@ -69,6 +70,64 @@ def counter_per_dispatch(path: str, counter: str):
     return {key: sum(v) / len(v) for key, v in agg.items()}
 
 
+def counters_per_dispatch(path: str):
+    """Every counter of a `--pmc` database, averaged per dispatch of each kernel shape."""
+    db = sqlite3.connect(path)
+    rows = db.execute("select kernel_name, grid_size, workgroup_size, counter_name, value from counters_collection")
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    for name, g, w, c, v in rows:
+        k, n = _short(name)
+        agg[(k, n, g // max(w, 1), w)][c].append(v)
+    return {key: {c: sum(v) / len(v) for c, v in cs.items()} for key, cs in agg.items()}
+
+
+CU_NUM = 256
+XCD_NUM = 8  # GRBM_GUI_ACTIVE comes summed over the XCDs: 8 x the dispatch's clock cycles
+
+
+def sq_lines(paths):
+    """Shader-sequencer counters of the pair kernels and the ratios read from them.  SQ_WAVE_CYCLES,
+    SQ_ACTIVE_INST_ANY and the SQ_WAIT_* counters are quad-cycles summed over the waves (their
+    ratios are shares of a wave's lifetime); SQ_INSTS_* count instructions; GRBM_GUI_ACTIVE / 8 is
+    the dispatch's length in clock cycles."""
+    merged = collections.defaultdict(dict)
+    for p in paths:
+        for key, cs in counters_per_dispatch(p).items():
+            merged[key].update(cs)
+    out = ["", "shader counters (--pmc SQ_*, GRBM_GUI_ACTIVE; per dispatch)"]
+    for key in sorted(merged):
+        k, n, wg, wx = key
+        if not k.startswith(("pair_", "rotate_")):
+            continue
+        c = merged[key]
+        out.append(f"  {k} N={n} WGs={wg} threads={wx}")
+        for name in sorted(c):
+            out.append(f"    {name:24s} {c[name]:16.6g}")
+        ratios = []
+        gui = c.get("GRBM_GUI_ACTIVE")
+        if gui:
+            cycles = gui / XCD_NUM
+            simd_cycles = 4 * CU_NUM * cycles
+            ratios.append(f"dispatch length {cycles:.4g} cycles")
+            if "SQ_INSTS_VALU" in c:
+                ratios.append(f"VALU instructions per SIMD per cycle {c['SQ_INSTS_VALU'] / simd_cycles:.3f} (a wave64 "
+                              f"fp32 instruction takes 2 cycles: limit 0.5)")
+            if "SQ_INSTS_LDS" in c:
+                ratios.append(f"LDS instructions per CU per cycle {c['SQ_INSTS_LDS'] / (CU_NUM * cycles):.3f}")
+            if "SQ_LDS_BANK_CONFLICT" in c:
+                ratios.append(f"LDS bank-conflict stall cycles per CU cycle "
+                              f"{c['SQ_LDS_BANK_CONFLICT'] / (CU_NUM * cycles):.3f}")
+        wc = c.get("SQ_WAVE_CYCLES")
+        if wc:
+            for name, label in (("SQ_ACTIVE_INST_ANY", "issuing"), ("SQ_WAIT_INST_ANY", "waiting to issue"),
+                                ("SQ_WAIT_INST_LDS", "waiting to issue LDS"),
+                                ("SQ_WAIT_ANY", "waiting on a dependency or barrier")):
+                if name in c:
+                    ratios.append(f"share of wave time {label} {c[name] / wc:.3f}")
+        out += [f"    -> {r}" for r in ratios]
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
@@ -78,6 +137,8 @@ def main() -> int:
     ap.add_argument("--copy-write")
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--top", type=int, default=0, help="list only the kernels with the largest total time")
+    ap.add_argument("--sq", action="append", default=[],
+                    help="a `--pmc` database of shader-sequencer counters (repeatable: one per pass)")
     ap.add_argument("--bench-json", help="JSON line printed by the profiled bench run: its source_digest is "
                                          "recorded (default: the digest of the sources as they are now)")
     args = ap.parse_args()
@@ -124,6 +185,8 @@ def main() -> int:
             out.append(f"  {k:28s} {n:6d} {wg:6d} {fetch[key]:11.1f} {write[key]:11.1f} {b:12.4g}")
             if k.startswith(("pair_", "rotate_")):
                 traffic["bytes"][f"{k}|{n}/{wg}"] = b
+    if args.sq:
+        out += sq_lines(args.sq)
     print("\n".join(out))
     if traffic is not None:
         print("TRAFFIC_JSON " + json.dumps(traffic, sort_keys=True))
