@@ -240,6 +240,10 @@ def held_clock_mhz(run_for_ms):
 
     import torch
 
+    if any(k.startswith("ROCPROF") for k in os.environ):
+        # under rocprofv3 every child process loads the profiler, which starts the GPU runtime
+        # before rocm-smi's interpreter is exec'd: no clock probe in profiled runs
+        return None
     run_for_ms()
     try:
         res = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=30)
