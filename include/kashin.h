@@ -69,8 +69,9 @@ int kashin_signs(int32_t n, uint64_t seed, int8_t* eps_host);
 
 /* Create a plan for vectors of length n, sign mask from `sign_seed`, and `iters` blocks of
  * Alg. 2 (each block = two u-steps and two vhat-steps).  Builds the FFT twiddle table and
- * the eps-folded frequency table on the current HIP device (the only device allocation of
- * this library).  Requires n even, kashin_supported_n(n), iters >= 1. */
+ * the eps-folded frequency table on the current HIP device (the library's only lasting device
+ * allocation; kashin_optq_factor's temporaries are freed before it returns).  Requires n even,
+ * kashin_supported_n(n), iters >= 1. */
 int kashin_plan(kashin_plan_t* out, int32_t n, uint64_t sign_seed, int32_t iters);
 
 /* Free a plan.  The caller must have synchronised every stream that used it. */
@@ -253,7 +254,8 @@ int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, in
 int kashin_optq_factor(const float* h, int32_t d, int64_t ldh, double damp, double* u, double* v, void* stream);
 
 /* Device workspace bytes kashin_optq_quantize needs for d_in rows of length n in chunks of `chunk`
- * (an error matrix, chunk x n fp32, and a factor block, chunk x d_in fp32); -1 for bad sizes. */
+ * (an error matrix, chunk x n fp32, and a factor block, chunk x d_in fp32); -1 for bad sizes
+ * (d_in < 0, n < 1, chunk outside [1, 128]). */
 int64_t kashin_optq_workspace_bytes(int64_t d_in, int32_t n, int32_t chunk);
 
 /* Quantise rows 0 .. quantize_rows - 1 of w_t (d_in rows, fp32, leading dimension ldw >= n = the

@@ -4,7 +4,8 @@
 
 Each kernel translation unit (one per supported vector length) compiles in
 parallel; objects go to ``_build/`` next to this file and the library to
-``libkashin.so`` in this package directory.
+``libkashin.so`` in this package directory.  The C consumer of the ABI that the
+tests run (tests/c_abi/kashin_abi_check.c) is built into ``_build/`` after it.
 """
 from __future__ import annotations
 
@@ -97,6 +98,29 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     return LIB
 
 
+# A C program that uses the library through include/kashin.h and the HIP runtime alone (the tests
+# run it): the boundary exercised without the Python binding.
+ABI_CHECK_SRC = os.path.join(ROOT, "tests", "c_abi", "kashin_abi_check.c")
+ABI_CHECK = os.path.join(BUILD, "kashin_abi_check")
+
+
+def build_abi_check(verbose: bool = False) -> str:
+    """Compile tests/c_abi/kashin_abi_check.c with the host C compiler against libkashin.so."""
+    os.makedirs(BUILD, exist_ok=True)
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        raise RuntimeError("no C compiler")
+    cmd = [cc, "-O1", "-std=c11", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+           "-I", "/opt/rocm/include", ABI_CHECK_SRC, "-o", ABI_CHECK, "-L", HERE, "-lkashin", "-L/opt/rocm/lib",
+           "-lamdhip64", "-lm", "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath,/opt/rocm/lib"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"C ABI check failed to build:\n{res.stderr}")
+    return ABI_CHECK
+
+
 # Host-code sanitizers for the C-ABI layer (device code is built without them: the GPU runs no
 # sanitizer).  Each -fsanitize= follows -Xarch_host, so only the host pass sees it.
 HOST_SANITIZE = "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split()
@@ -140,3 +164,4 @@ if __name__ == "__main__":
         print(build_host_sanitized(verbose="-v" in sys.argv))
     else:
         print(build(verbose="-v" in sys.argv))
+        print(build_abi_check(verbose="-v" in sys.argv))

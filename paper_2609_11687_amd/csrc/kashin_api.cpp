@@ -603,7 +603,7 @@ int kashin_optq_factor(const float* h, int32_t d, int64_t ldh, double damp, doub
 }
 
 int64_t kashin_optq_workspace_bytes(int64_t d_in, int32_t n, int32_t chunk) {
-  if (d_in < 0 || n < 1 || chunk < 1) return -1;
+  if (d_in < 0 || n < 1 || chunk < 1 || chunk > kashin::kOptqMaxChunk) return -1;
   return kashin::optq_workspace_bytes(d_in, n, chunk);
 }
 

@@ -3,6 +3,7 @@ computes the sign mask like the oracle, and rejects bad arguments before touchin
 import ctypes
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -265,3 +266,19 @@ def test_optq_entry_points_validate_before_device():
     args = (buf, 4, 512, buf, buf, 4, 4, 8, 0, 0, buf, buf, buf, buf, buf, 1 << 20, None)
     assert L.kashin_optq_quantize(fake, *args) == K.KASHIN_E_INVALID
     assert "plan" in L.kashin_last_error().decode()
+
+
+def _abi_check_binary():
+    from paper_2609_11687_amd import build as B
+
+    if not os.path.exists(B.ABI_CHECK) or os.path.getmtime(B.ABI_CHECK) < os.path.getmtime(B.ABI_CHECK_SRC):
+        B.build_abi_check()
+    return B.ABI_CHECK
+
+
+def test_c_program_uses_the_abi_host_side():
+    """A C program linked against libkashin.so with include/kashin.h alone: the supported-length
+    set, the sign mask against published splitmix64 outputs, validation and error messages."""
+    res = subprocess.run([_abi_check_binary(), "host"], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.strip().endswith("ok")
