@@ -445,6 +445,7 @@ def fig2(args) -> int:
             self.run = f
 
     ms_per_step, launch_ms = time_launches([_L(f) for f in launches], args.steps, args.warmup, stream)
+    baseline = None if args.no_cpu_baseline else fig2_cpu_baseline(x[:1], n)
     result = {
         "metric": "Fig. 2 set-up: residual after greedy updates, Alg. 2 vs Alg. 1, N = 10^4",
         "value": 2 * rows / (ms_per_step / 1e3),
@@ -456,8 +457,59 @@ def fig2(args) -> int:
                    "ms_alternating": launch_ms[0], "ms_original": launch_ms[1]},
         "fig2": out,
     }
+    if baseline is not None:
+        result["cpu_baseline"] = baseline
     print(json.dumps(result), flush=True)
     return 0
+
+
+def fig2_cpu_baseline(x0, n, steps: int = 24):
+    """The oracle on vector 0 of the Fig. 2 set-up, both schedules, the first `steps` updates: its
+    rate, and the GPU's factors after those updates (traced with a plan of steps / 4 blocks)
+    against the oracle replayed on the GPU's near-tie decisions (signs within 1e-6 ||x||_inf of
+    zero, choices within 1e-5 of a tie).  24 updates leave a residual near 1e-5 of ||x||_2: once it
+    nears fp32's resolution of x (after about 32), the two residuals share no more digits and
+    Alg. 1's half choices, decided by comparing two l1 norms of that residual, no longer need to
+    agree (the factors, then changed by steps of that size, still do)."""
+    import numpy as np
+    import torch
+
+    import oracle.kashin_ref as ref
+    from paper_2609_11687_amd import kashin as K
+
+    dev = x0.device
+    k = steps // 4
+    plan = K.kashin_plan(n, 0, k)
+    x64 = x0.double().cpu().numpy()
+    winf = float(np.abs(x64).max())
+    eps = ref.sign_mask(n, 0)
+    ref.dct2_matrix(n)  # the dense cosine matrix, built outside the timing
+    rows_t = torch.zeros(1, dtype=torch.int64, device=dev)
+    parity, seconds = {}, 0.0
+    for sched in ("alternating", "original"):
+        sg = torch.empty((1, 4 * k, n), dtype=torch.int8, device=dev)
+        cs = torch.empty((1, 4 * k), dtype=torch.float32, device=dev)
+        ch = torch.empty((1, 4 * k), dtype=torch.int8, device=dev)
+        r2 = torch.empty((1, 4 * k), dtype=torch.float32, device=dev)
+        ut, vt = torch.empty_like(x0), torch.empty_like(x0)
+        K.kashin_trace_schedule(plan, sched, x0, rows_t, sg, cs, ch, r2, ut, vt)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rep = ref.decompose_schedule(x64, eps, 4 * k, sched, replay_signs=sg.cpu().numpy(),
+                                     replay_choices=ch.cpu().numpy(), tau=1e-6 * winf, choice_band=1e-5)
+        seconds += time.perf_counter() - t0
+        parity[sched] = {
+            "updates": 4 * k,
+            "max_du": float(np.abs(ut.double().cpu().numpy() - rep["u"]).max() / winf),
+            "max_dv": float(np.abs(vt.double().cpu().numpy() - rep["vhat"]).max() / winf),
+            "outside_tie_band": int(np.asarray(rep["replay_outside"]).sum()),
+            "choices_outside_band": int(np.asarray(rep["choice_outside"]).sum()),
+            "tolerance_factors": 1e-4,
+        }
+    return {"value": 2 / seconds, "unit": "vectors/s", "cores": int(_blas_threads()), "kind": "oracle",
+            "sample": f"vector 0, {4 * k} updates of each schedule, float64 dense P (N = {n}); {seconds:.1f} s; "
+                      f"cosine-matrix construction excluded",
+            "parity": parity}
 
 
 def main() -> int:
