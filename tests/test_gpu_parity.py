@@ -1018,6 +1018,35 @@ def _replaying_quantiser(plan, eps, k, record, codes_u, codes_v, n):
     return quantiser
 
 
+@pytest.mark.parametrize("lloyd,exact", [(0, False), (2, False), (2, True)])
+def test_optq_single_chunk_is_plain_quantisation(lloyd, exact):
+    """With one chunk covering every column nothing is carried: kashin_optq_quantize must give
+    kashin_quantize's codes and centres (Lloyd passes included) and kashin_reconstruct's rows bit
+    for bit, and leave w_t as it was (the exact form carries inside the chunk, so only its first
+    column is plain quantisation and the rest differ)."""
+    from paper_2609_11687_amd import optq
+
+    d_in, n = 64, 512
+    rng = np.random.default_rng(5 + lloyd)
+    w = _rows(rng, d_in, n, "t4")
+    h = ref.synthetic_hessian(d_in, 200, 3, outlier_cols=2, outlier_scale=5.0).astype(np.float32)
+    plan = K.kashin_plan(n, 77, 12)
+    w_t = pu.to_dev(w)
+    cu, cv, ce, q_t = optq.optq_quantize(plan, w_t, pu.to_dev(h), 128, lloyd_iters=lloyd, exact=exact)
+    # the exact form quantises its first column alone (no partner row in its complex FFT)
+    ref_rows = 1 if exact else d_in
+    rcu, rcv, rce = K.quantize_alloc(plan, pu.to_dev(w[:ref_rows]), lloyd)
+    rq = torch.empty((ref_rows, n), dtype=torch.float32, device="cuda")
+    K.kashin_reconstruct(plan, rcu, rcv, rce, rq)
+    torch.cuda.synchronize()
+    for got, want in ((cu, rcu), (cv, rcv), (ce, rce), (q_t, rq)):
+        np.testing.assert_array_equal(got[:ref_rows].cpu().numpy(), want.cpu().numpy())
+    if exact:
+        assert not np.array_equal(w_t.cpu().numpy()[1:], w[1:])  # later columns were compensated
+    else:
+        np.testing.assert_array_equal(w_t.cpu().numpy(), w)
+
+
 @pytest.mark.parametrize("chunk,exact", [(32, False), (32, True), (1, False)])
 def test_optq_pipeline_end_to_end(chunk, exact):
     """The whole compensated pipeline against ref.optq_kashin: the final dequantised Q and the
