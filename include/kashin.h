@@ -48,7 +48,9 @@ enum {
   KASHIN_E_HIP = -4,           /* HIP runtime error (no device, launch failure, ...) */
 };
 
-enum { KASHIN_F32 = 0, KASHIN_F16 = 1 };
+/* Input element types of the weight rows (every computation is fp32): IEEE binary32, binary16,
+ * and bfloat16 (the upper half of a binary32; widened exactly). */
+enum { KASHIN_F32 = 0, KASHIN_F16 = 1, KASHIN_BF16 = 2 };
 
 /* 1 if vectors of length n have a compiled kernel, else 0.  Host only, no device needed.
  * The supported lengths are exactly
@@ -83,8 +85,8 @@ int kashin_plan_signs(kashin_plan_t plan, int8_t* eps_host);
 /* Plan properties (host). */
 int kashin_plan_info(kashin_plan_t plan, int32_t* n, int32_t* iters, uint64_t* seed);
 
-/* Alg. 2 on every row of w (m x n, leading dimension ldw >= n, dtype KASHIN_F32 or
- * KASHIN_F16; arithmetic is fp32).  Outputs, all fp32 row-major with leading dimension n:
+/* Alg. 2 on every row of w (m x n, leading dimension ldw >= n, dtype KASHIN_F32, KASHIN_F16 or
+ * KASHIN_BF16; arithmetic is fp32).  Outputs, all fp32 row-major with leading dimension n:
  *   u, vhat   m x n  factors with w = u + P vhat + r                       (required)
  *   r         m x n  residual after the last block (costs one more P)      (nullable)
  *   cstep     m x 4  magnitudes c of the four steps of block 0: c1, c2 (u-steps) and
@@ -203,7 +205,7 @@ int kashin_trace_schedule(kashin_plan_t plan, int32_t schedule, float tol, const
  * output of `seed` is set (the generator of kashin_signs).  R is orthogonal.
  * y = R x (inverse = 0) or y = R^T x (inverse = 1) for m rows.
  *   n       odd part b in {1, 3, 43}, n <= 16384 (else KASHIN_E_UNSUPPORTED_N)
- *   x       m rows, dtype KASHIN_F32 or KASHIN_F16, leading dimension ldx >= n (device)
+ *   x       m rows, dtype KASHIN_F32, KASHIN_F16 or KASHIN_BF16, leading dimension ldx >= n (device)
  *   y       m fp32 rows, leading dimension ldy >= n (device); y == x is allowed (in place) for
  *           fp32 with ldy == ldx, any other overlap is KASHIN_E_INVALID
  * Plan-free: runs on the current device.  Quantising R w and reconstructing R^T w_hat

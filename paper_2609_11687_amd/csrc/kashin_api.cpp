@@ -50,6 +50,8 @@ int ok() {
   return KASHIN_OK;
 }
 
+bool dtype_ok(int32_t dtype) { return dtype == KASHIN_F32 || dtype == KASHIN_F16 || dtype == KASHIN_BF16; }
+
 bool live(const kashin_plan_s* p) {
   std::lock_guard<std::mutex> lk(g_plans_mu);
   return p != nullptr && g_plans.count(p) != 0;
@@ -240,7 +242,7 @@ int kashin_decompose(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m
                      float* vhat, float* r, float* cstep, float* bounds, void* stream) {
   int st = check_common(plan, m);
   if (st) return st;
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (m == 0) return ok();
   if (!w || !u || !vhat) return fail(KASHIN_E_INVALID, "w, u and vhat must be non-null");
@@ -261,7 +263,7 @@ int kashin_quantize(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m,
                     uint8_t* codes_u, uint8_t* codes_v, float* centers, void* stream) {
   int st = check_common(plan, m);
   if (st) return st;
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
   if (m == 0) return ok();
@@ -283,7 +285,7 @@ int kashin_quantize_grouped(const kashin_quantize_item* items, int32_t count, in
   if (count < 0) return fail(KASHIN_E_INVALID, "count must be >= 0 (got %d)", count);
   if (count == 0) return ok();
   if (items == nullptr) return fail(KASHIN_E_INVALID, "items is null");
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
   const kashin_plan_s* p0 = nullptr;
   for (int32_t i = 0; i < count; ++i) {
@@ -335,7 +337,7 @@ int kashin_trace(kashin_plan_t plan, const void* w, int32_t dtype, int64_t m, in
                  int64_t nrows, int8_t* sign_trace, float* c_trace, float* u, float* vhat, void* stream) {
   int st = check_common(plan, m);
   if (st) return st;
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (nrows < 0) return fail(KASHIN_E_INVALID, "nrows must be >= 0");
   if (nrows == 0 || m == 0) return ok();
@@ -370,7 +372,7 @@ int kashin_decompose_schedule(kashin_plan_t plan, int32_t schedule, float tol, c
   if (st) return st;
   st = check_schedule(schedule, tol);
   if (st) return st;
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (m == 0) return ok();
   if (!w || !u || !vhat) return fail(KASHIN_E_INVALID, "w, u and vhat must be non-null");
@@ -394,7 +396,7 @@ int kashin_trace_schedule(kashin_plan_t plan, int32_t schedule, float tol, const
   if (st) return st;
   st = check_schedule(schedule, tol);
   if (st) return st;
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (nrows < 0) return fail(KASHIN_E_INVALID, "nrows must be >= 0");
   if (nrows == 0 || m == 0) return ok();
@@ -440,7 +442,7 @@ int kashin_quantize_rotated(kashin_plan_t plan, uint64_t rot_seed, const void* w
   if (st) return st;
   if (!kashin::rotate_supported_n(plan->n))
     return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", plan->n);
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (ldw < plan->n) return fail(KASHIN_E_INVALID, "ldw (%lld) < n (%d)", (long long)ldw, plan->n);
   if (lloyd_iters < 0) return fail(KASHIN_E_INVALID, "lloyd_iters must be >= 0");
   if (m == 0) return ok();
@@ -483,13 +485,13 @@ int kashin_rotate(int32_t n, uint64_t seed, int32_t inverse, const void* x, int3
   if (!kashin::rotate_supported_n(n))
     return fail(KASHIN_E_UNSUPPORTED_N, "n = %d: the rotation needs n <= 16384 with odd part 1, 3 or 43", n);
   if (inverse != 0 && inverse != 1) return fail(KASHIN_E_INVALID, "inverse must be 0 or 1");
-  if (dtype != KASHIN_F32 && dtype != KASHIN_F16) return fail(KASHIN_E_INVALID, "dtype must be F32 or F16");
+  if (!dtype_ok(dtype)) return fail(KASHIN_E_INVALID, "dtype must be F32, F16 or BF16");
   if (m < 0) return fail(KASHIN_E_INVALID, "m must be >= 0 (got %lld)", (long long)m);
   if (ldx < n || ldy < n) return fail(KASHIN_E_INVALID, "ldx (%lld) and ldy (%lld) must be >= n (%d)", (long long)ldx,
                                       (long long)ldy, n);
   if (m == 0) return ok();
   if (!x || !y) return fail(KASHIN_E_INVALID, "x and y must be non-null");
-  const size_t esz = dtype == KASHIN_F16 ? 2 : 4;
+  const size_t esz = dtype == KASHIN_F32 ? 4 : 2;
   const uintptr_t x0 = reinterpret_cast<uintptr_t>(x), y0 = reinterpret_cast<uintptr_t>(y);
   const uintptr_t x1 = x0 + ((m - 1) * ldx + n) * esz, y1 = y0 + ((m - 1) * ldy + n) * 4;
   const bool in_place = x0 == y0 && dtype == KASHIN_F32 && ldx == ldy;

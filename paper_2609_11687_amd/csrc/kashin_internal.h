@@ -7,6 +7,14 @@
 
 namespace kashin {
 
+// bfloat16 input (KASHIN_BF16): the upper 16 bits of an IEEE binary32, widened exactly by a shift
+struct bf16_t {
+  uint16_t bits;
+};
+__device__ inline float bf16_to_f32(bf16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
+}
+
 enum Mode : int32_t {
   MODE_DECOMPOSE = 0,  // write u, vhat (+ r, cstep, bounds)
   MODE_QUANTIZE = 1,   // fused decompose + cluster + pack, write codes and centres only

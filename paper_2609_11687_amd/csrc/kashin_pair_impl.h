@@ -28,6 +28,7 @@
 #include <cstdint>
 #include <type_traits>
 
+#include "kashin.h"
 #include "kashin_internal.h"
 #include "kashin_rot_impl.h"
 #include "kashin_tables.h"
@@ -1228,6 +1229,7 @@ __device__ __forceinline__ float2 greedy_step(float2 (&z)[C::E], float2 (&acc)[C
 // ------------------------------------------------------------------ loads / stores
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(__half v) { return __half2float(v); }
+__device__ __forceinline__ float to_f32(bf16_t v) { return bf16_to_f32(v); }
 
 // Load rows a (and b if >= 0) into the greedy register layout, in even/odd order.
 // `tid` is the thread index (a laundered copy in loops whose other values are invariant, so
@@ -1313,7 +1315,8 @@ __device__ __forceinline__ void load_pair_staged(const void* w, int dtype, int64
                                                  uint64_t seed, float scale, float2* lds, F&& f) {
   const int tid = bfly<C>(threadIdx.x);
   __syncthreads();
-  if (dtype == 1) stage_pair_t<C, ROT>(lds, static_cast<const __half*>(w), ldw, ra, rb, seed, tid);
+  if (dtype == KASHIN_F16) stage_pair_t<C, ROT>(lds, static_cast<const __half*>(w), ldw, ra, rb, seed, tid);
+  else if (dtype == KASHIN_BF16) stage_pair_t<C, ROT>(lds, static_cast<const bf16_t*>(w), ldw, ra, rb, seed, tid);
   else stage_pair_t<C, ROT>(lds, static_cast<const float*>(w), ldw, ra, rb, seed, tid);
   __syncthreads();
   if constexpr (ROT) {
@@ -1328,7 +1331,8 @@ __device__ __forceinline__ void load_pair_staged(const void* w, int dtype, int64
 template <class C>
 __device__ __forceinline__ void load_pair(float2 (&z)[C::E], const void* w, int dtype, int64_t ldw, int64_t ra,
                                           int64_t rb, int tid = bfly<C>(threadIdx.x)) {
-  if (dtype == 1) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, tid);
+  if (dtype == KASHIN_F16) load_pair_t<C>(z, static_cast<const __half*>(w), ldw, ra, rb, tid);
+  else if (dtype == KASHIN_BF16) load_pair_t<C>(z, static_cast<const bf16_t*>(w), ldw, ra, rb, tid);
   else load_pair_t<C>(z, static_cast<const float*>(w), ldw, ra, rb, tid);
 }
 

@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdint>
 
+#include "kashin.h"
 #include "kashin_internal.h"
 #include "kashin_rot_impl.h"
 
@@ -26,6 +27,7 @@ constexpr int kPadMaxN = 8192;
 
 __device__ __forceinline__ float load_f32(const float* p) { return *p; }
 __device__ __forceinline__ float load_f32(const __half* p) { return __half2float(*p); }
+__device__ __forceinline__ float load_f32(const bf16_t* p) { return bf16_to_f32(*p); }
 
 template <int B, bool INV, bool PAD, class IT>
 __global__ __launch_bounds__(kRotThreads) void rotate_kernel(int n, uint64_t seed, float scale, const IT* x,
@@ -109,8 +111,10 @@ bool rotate_supported_n(int n) {
 
 hipError_t launch_rotate(int n, uint64_t seed, bool inverse, const void* x, int dtype, int64_t ldx, float* y,
                          int64_t ldy, int64_t m, hipStream_t stream) {
-  if (dtype == 1)
+  if (dtype == KASHIN_F16)
     return launch_rot_odd(n, seed, inverse, static_cast<const __half*>(x), ldx, y, ldy, m, stream);
+  if (dtype == KASHIN_BF16)
+    return launch_rot_odd(n, seed, inverse, static_cast<const bf16_t*>(x), ldx, y, ldy, m, stream);
   return launch_rot_odd(n, seed, inverse, static_cast<const float*>(x), ldx, y, ldy, m, stream);
 }
 

@@ -20,6 +20,7 @@ KASHIN_E_NOMEM = -3
 KASHIN_E_HIP = -4
 KASHIN_F32 = 0
 KASHIN_F16 = 1
+KASHIN_BF16 = 2
 
 EXPORTS = (
     "kashin_supported_n", "kashin_signs", "kashin_plan", "kashin_plan_destroy", "kashin_plan_signs",
@@ -111,6 +112,8 @@ def _dtype_code(t) -> int:
         return KASHIN_F32
     if t.dtype == torch.float16:
         return KASHIN_F16
+    if t.dtype == torch.bfloat16:
+        return KASHIN_BF16
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
@@ -248,7 +251,7 @@ def kashin_plan_info(plan: Plan):
 # ----------------------------------------------------------------------------- device calls
 def kashin_decompose(plan, w, u, vhat, r=None, cstep=None, bounds=None, stream=None):
     import torch
-    m, ldw = _need_rows(plan, w, plan.n, "w", (torch.float32, torch.float16))
+    m, ldw = _need_rows(plan, w, plan.n, "w", (torch.float32, torch.float16, torch.bfloat16))
     for name, t, nl in (("u", u, False), ("vhat", vhat, False), ("r", r, True)):
         _need(plan, t, (m, plan.n), torch.float32, name, nullable=nl)
     _need(plan, cstep, (m, 4), torch.float32, "cstep", nullable=True)
@@ -372,7 +375,7 @@ def kashin_reconstruct_rotated(plan, rot_seed, codes_u, codes_v, centers, w_hat,
 
 
 def kashin_rotate(n, seed, x, y, inverse=False, stream=None):
-    """y = R x (or R^T x) row-wise; x fp32 or fp16 rows, y fp32 rows (y may be x, fp32)."""
+    """y = R x (or R^T x) row-wise; x fp32, fp16 or bf16 rows, y fp32 rows (y may be x, fp32)."""
     m, ldx = _need_rows(None, x, n, "x")
     my, ldy = _need_rows(None, y, n, "y", (_f32(),))
     if my != m:

@@ -282,3 +282,18 @@ def test_c_program_uses_the_abi_host_side():
     res = subprocess.run([_abi_check_binary(), "host"], capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
     assert res.stdout.strip().endswith("ok")
+
+
+def test_input_dtype_codes():
+    """F32, F16 and BF16 are the input element types; any other code is rejected before a launch
+    with a message naming the three (the pointers are never dereferenced)."""
+    L = K.lib()
+    assert (K.KASHIN_F32, K.KASHIN_F16, K.KASHIN_BF16) == (0, 1, 2)
+    p = ctypes.c_void_p(0x1000)
+    assert L.kashin_rotate(512, 0, 0, p, 3, 4, 512, p, 512, None) == K.KASHIN_E_INVALID
+    assert "BF16" in L.kashin_last_error().decode()
+    import torch
+
+    assert K._dtype_code(torch.zeros(1, dtype=torch.bfloat16)) == K.KASHIN_BF16
+    with pytest.raises(TypeError):
+        K._dtype_code(torch.zeros(1, dtype=torch.float64))

@@ -377,6 +377,53 @@ def test_fp16_input_equals_fp32_of_same_values():
     np.testing.assert_array_equal(a[1].cpu().numpy(), b[1].cpu().numpy())
 
 
+@pytest.mark.parametrize("n", [512, 4096, 11008])
+def test_bf16_input_equals_fp32_of_same_values(n):
+    """bfloat16 rows (widened exactly) give what fp32 rows of the same values give, bit for bit, in
+    every entry point that reads weight rows: decompose (u, vhat, r), quantize (plain, grouped,
+    rotated), trace, the schedules and the rotation (odd row count: an unpaired last row)."""
+    k, m = 6, 5
+    rng = np.random.default_rng(n + 8)
+    wb = torch.from_numpy(_rows(rng, m, n, "t4")).to(torch.bfloat16).cuda()
+    wf = wb.float()
+    plan = K.kashin_plan(n, 21, k)
+    outs = []
+    for w in (wb, wf):
+        r = {}
+        u, vh = torch.empty((m, n), device="cuda"), torch.empty((m, n), device="cuda")
+        rr = torch.empty_like(u)
+        K.kashin_decompose(plan, w, u, vh, rr)
+        r["decompose"] = (u, vh, rr)
+        r["quantize"] = K.quantize_alloc(plan, w, 1)
+        nb = (n + 3) // 4
+        g = (torch.empty((m, nb), dtype=torch.uint8, device="cuda"), torch.empty((m, nb), dtype=torch.uint8,
+             device="cuda"), torch.empty((m, 2, 4), device="cuda"))
+        K.kashin_quantize_grouped([(plan, w) + g], 0)
+        r["grouped"] = g
+        rows = torch.arange(m, dtype=torch.int64, device="cuda")
+        sg = torch.empty((m, 4 * k, n), dtype=torch.int8, device="cuda")
+        ct = torch.empty((m, 4 * k), device="cuda")
+        ut, vt = torch.empty_like(u), torch.empty_like(u)
+        K.kashin_trace(plan, w, rows, sg, ct, ut, vt)
+        r["trace"] = (sg, ct, ut, vt)
+        us, vs = torch.empty_like(u), torch.empty_like(u)
+        K.kashin_decompose_schedule(plan, "adaptive", w, us, vs)
+        r["schedule"] = (us, vs)
+        y = torch.empty_like(u)
+        K.kashin_rotate(n, 5, w, y)
+        r["rotate"] = (y,)
+        cr = (torch.empty((m, nb), dtype=torch.uint8, device="cuda"), torch.empty((m, nb), dtype=torch.uint8,
+              device="cuda"), torch.empty((m, 2, 4), device="cuda"))
+        K.kashin_quantize_rotated(plan, 5, w, 0, *cr)
+        r["rotated"] = cr
+        torch.cuda.synchronize()
+        outs.append({key: [t.cpu().numpy() for t in v] for key, v in r.items()})
+    assert outs[0].keys() == outs[1].keys()
+    for key in outs[0]:
+        for a_, b_ in zip(outs[0][key], outs[1][key]):
+            np.testing.assert_array_equal(a_, b_, err_msg=key)
+
+
 # one length per transform shape: generic (256), lane-paired resident (512, 4096), odd inner pass
 # (768), palindromic resident (1024, 16384), split radix-43 (11008)
 @pytest.mark.parametrize("n", [256, 512, 768, 1024, 3072, 4096, 11008, 16384])
