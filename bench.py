@@ -860,6 +860,10 @@ def main() -> int:
         "roofline": roofline,
         "source_digest": source_digest(),
     }
+    if args.op in ("quantize", "quantize_h", "schedule", "rotate"):
+        # GB/s of weights quantised: the stored weight bytes the step reads, per second
+        wbytes = wl.layers * sum(sp.rows * sp.n * (2 if sp.dtype == "f16" else 4) for sp in wl.matrices)
+        result["weights_gbps"] = wbytes / (ms_per_step / 1e3) / 1e9
     if args.op == "schedule":
         # convergence (Fig. 2 style): ||rho||_2 / ||w||_2 after 4, 8, 16 and 32 atomic steps, the
         # mean over the first 8 rows of the first matrix (recorded by kashin_trace_schedule)
