@@ -525,6 +525,10 @@ def main() -> int:
     ap.add_argument("--exact", action="store_true", help="--op optq: columns one at a time inside each chunk")
     ap.add_argument("--matrix", default="q_proj", help="matrix of the workload (--op optq)")
     ap.add_argument("--chunk", type=int, default=128, help="columns per compensation chunk (--op optq)")
+    ap.add_argument("--model-layers", type=int, default=0,
+                    help="--op optq --matrix all: one step = this many layers, each factorising its four "
+                         "Hessians (inputs of q/k/v, o, gate/up, down) inside the timed region, then the "
+                         "compensated quantisation of its seven matrices")
     ap.add_argument("--schedule", choices=("alternating", "reverse", "adaptive", "original"), default="adaptive")
     ap.add_argument("--lloyd", type=int, default=0)
     ap.add_argument("--per-matrix", action="store_true",
@@ -730,12 +734,28 @@ def main() -> int:
             for *_, st in jobs:
                 s.wait_stream(st)
 
+        if args.model_layers > 0:
+            if args.matrix != "all":
+                raise SystemExit("--model-layers needs --matrix all")
+            one_layer = run_optq
+            widths = sorted(hess_by_din)
+
+            def run_optq(s):  # noqa: F811 - the model: every layer factorises its Hessians, then quantises
+                for _ in range(args.model_layers):
+                    for d_in in widths:
+                        # three distinct inputs of width 4096 per layer (q/k/v, o, gate/up), one of 11008
+                        for _rep in range(3 if d_in == widths[0] and len(widths) > 1 else 1):
+                            factors[d_in] = optq.compensation_factor(hess_by_din[d_in], want_v=not args.exact)
+                    one_layer(s)
+
         # one launch covers every matrix: its length is the matrices' common d_out, else 0 (mixed)
         d_outs = {j[1].shape[1] for j in jobs}
         d_out = d_outs.pop() if len(d_outs) == 1 else 0
-        cols = sum(j[1].shape[0] for j in jobs)
-        flops = sum(j[1].shape[0] * counted_flops_per_vector(j[1].shape[1], wl.iters) for j in jobs) + gemm
-        launches.append(Launch(d_out, cols, flops, sum(j[1].numel() * 12 for j in jobs), run_optq, kind="optq"))
+        reps = max(1, args.model_layers)
+        cols = reps * sum(j[1].shape[0] for j in jobs)
+        flops = reps * (sum(j[1].shape[0] * counted_flops_per_vector(j[1].shape[1], wl.iters) for j in jobs) + gemm)
+        launches.append(Launch(d_out, cols, flops, reps * sum(j[1].numel() * 12 for j in jobs), run_optq,
+                               kind="optq"))
     else:
         g = torch.Generator(device=dev).manual_seed(0)
         for n in sorted({spec.n for spec in wl.matrices}):
@@ -781,6 +801,9 @@ def main() -> int:
                                                            for i in chosen)
                     + f" (chains on {n_streams} streams, {os.environ.get('GPU_MAX_HW_QUEUES')} hardware queues), columns quantised in chunks of {args.chunk}, k={wl.iters}, "
                     f"Hessian of 2 d_in seeded Gaussian activations with 0.1% outlier channels x20")
+        if args.model_layers > 0:
+            workload += (f"; one step = {args.model_layers} such layers (the same synthetic matrices), each "
+                         f"factorising four Hessians (3 at d_in 4096, 1 at 11008) inside the step")
     elif main_kind == "schedule":
         achieved = dom_flops / dom_s / 1e12
         roofline = {
